@@ -1,0 +1,203 @@
+/*
+ * ibp.h -- C ABI of the MI355X (gfx950) Invariant Bit Packing library.
+ *
+ * Invariant Bit Packing (arxiv 2605.30728, Sec. 4) stores, for each cluster of rows,
+ * the bit positions on which every row agrees once (Mask, and their values in Bitval)
+ * and packs only the remaining, variant bits of each row. This library uses clusters
+ * of `group_rows` consecutive rows (the clustered form of Sec. 6.5 with the threshold
+ * T equal to the cluster size, so a bit is invariant exactly when every row of the
+ * cluster agrees on it). Decompression rebuilds each 32-bit word of a row as
+ *     word = Bitval_w | deposit(next popcount(~Mask_w) packed bits, ~Mask_w)
+ * on the GPU (Sec. 4.3), fused with a row gather for embedding / feature lookups.
+ *
+ * Conventions for every call:
+ *   - Return value: an ibp_status; IBP_OK (0) on success. On any other value the call
+ *     wrote nothing to its outputs and enqueued nothing, and ibp_last_error() gives a
+ *     message (thread-local, valid until the next call on the same thread).
+ *   - Rows are opaque little-endian bytes (any element type); row_bytes must be a
+ *     positive multiple of 4 (32-bit chunks, the paper's 4-byte chunk size).
+ *   - Row ids are int64; an id outside [0, n_rows) is IBP_ERANGE (host ids).
+ *   - `stream` arguments are HIP streams (hipStream_t) passed as void*; NULL means
+ *     the device's null stream. Device work is asynchronous: results in device
+ *     memory are valid once that stream reaches the point where the call enqueued.
+ *   - A handle may be used by one host thread at a time (IBP_ESTATE otherwise).
+ *     Distinct handles are independent.
+ *
+ * Compressed stream layout (version 1, little-endian, no implicit padding):
+ *   [0,64)   header: "IBP1", u32 version=1, u32 row_bytes, u32 group_rows,
+ *            u64 n_rows, u64 n_groups=ceil(n_rows/group_rows), u32 flags=0,
+ *            u32 reserved=0, u64 meta_off=64, u64 index_off, u64 payload_off
+ *   meta     per group g: Mask_g[row_bytes] then Bitval_g[row_bytes]
+ *   index    u64 off[0..n_groups], off[0]=0, off[g+1]=off[g]+n_g*rb_g where
+ *            rb_g = row_bytes - floor(popcount(Mask_g)/8) (Fig. 4 size rule with no
+ *            participation bits: under T = cluster size every chunk matches Bitval)
+ *   payload  packed rows back to back: row r of group g starts at
+ *            payload_off + off[g] + r*rb_g; packed bit k is bit k%8 of byte k/8 and
+ *            holds the k-th variant bit of the row in ascending bit position
+ *            (row bit p = bit p%8 of byte p/8); padding bits are zero.
+ */
+#ifndef IBP_H
+#define IBP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    IBP_OK = 0,
+    IBP_EINVAL = 1,    /* a bad argument (null pointer, size, alignment, flag) */
+    IBP_ERANGE = 2,    /* a row id or row range outside the stream */
+    IBP_ENOMEM = 3,    /* host or device allocation failed, or an output is too small */
+    IBP_ECORRUPT = 4,  /* the stream failed validation */
+    IBP_EHIP = 5,      /* a HIP runtime error (sticky on a handle once seen) */
+    IBP_ESTATE = 6     /* the handle is in use by another thread, or closed */
+} ibp_status;
+
+typedef struct ibp_handle ibp_handle;   /* opaque, owned by the library */
+
+typedef struct {
+    uint64_t n_rows;
+    uint64_t n_groups;
+    uint64_t meta_off;       /* byte offsets inside the stream */
+    uint64_t index_off;
+    uint64_t payload_off;
+    uint64_t payload_bytes;  /* off[n_groups] */
+    uint64_t stream_bytes;   /* payload_off + payload_bytes */
+    uint32_t row_bytes;
+    uint32_t group_rows;
+} ibp_desc;
+
+typedef struct {
+    uint64_t calls;          /* decompress / gather calls that enqueued work */
+    uint64_t rows_out;       /* rows written to device outputs */
+    uint64_t out_bytes;      /* bytes written to device outputs */
+    uint64_t h2d_bytes;      /* bytes the calls moved host-to-device (ids, tables, payload) */
+    uint64_t h2d_payload_bytes; /* of which packed payload bytes */
+    uint64_t host_pack_ns;   /* host time spent gathering packed rows into staging */
+} ibp_stats;
+
+/* Open flags: where the packed payload lives after ibp_open. */
+enum {
+    IBP_OPEN_PAYLOAD_DEVICE = 0, /* copied to device memory (HBM) once, at open */
+    IBP_OPEN_PAYLOAD_HOST = 1    /* kept in library-owned pinned host memory; every call
+                                    moves the needed packed bytes over PCIe through
+                                    double-buffered staging on a side stream */
+};
+
+/*
+ * ibp_compress_bound -- an upper bound on the stream size of n_rows rows
+ * (every row stored raw plus the header, metadata and index). Host only.
+ * Errors: IBP_EINVAL for a null `bound`, row_bytes not a positive multiple of 4,
+ * group_rows == 0, or a size that overflows 64 bits.
+ */
+ibp_status ibp_compress_bound(uint64_t n_rows, uint32_t row_bytes, uint32_t group_rows,
+                              uint64_t *bound);
+
+/*
+ * ibp_compress -- compress n_rows rows (row-major, row_bytes each, at `rows`) in
+ * clusters of group_rows consecutive rows: per cluster, Mask/Bitval of the bits every
+ * row agrees on (Sec. 4.1 with T = cluster size), then each row's variant bits packed
+ * in ascending order (Sec. 4.2), into the version-1 stream above. Host only,
+ * synchronous, re-entrant. n_threads <= 0 uses every online CPU. The caller owns
+ * `rows` and `out`; *out_bytes receives the stream size (also when out_cap is too
+ * small, in which case IBP_ENOMEM is returned and `out` is untouched). The stream is
+ * a pure function of (rows, n_rows, row_bytes, group_rows).
+ * Errors: IBP_EINVAL (null pointers with n_rows > 0, bad row_bytes or group_rows),
+ * IBP_ENOMEM (out_cap too small or a host allocation failed).
+ */
+ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes,
+                        uint32_t group_rows, int n_threads, void *out, uint64_t out_cap,
+                        uint64_t *out_bytes);
+
+/*
+ * ibp_describe -- validate a stream and fill *d. Host only. Validation covers the
+ * header fields, the section offsets, Bitval being zero wherever Mask is zero, a
+ * monotone index with off[0] = 0 and off[g+1] - off[g] = n_g * rb_g, and the stream
+ * being at least payload_off + off[n_groups] bytes long.
+ * Errors: IBP_EINVAL (null pointers), IBP_ECORRUPT (any validation failure).
+ */
+ibp_status ibp_describe(const void *stream, uint64_t stream_bytes, ibp_desc *d);
+
+/*
+ * ibp_open -- validate `stream` (as ibp_describe) and load it for decompression on
+ * HIP device `device`: the metadata and index are copied to device memory, and the
+ * payload to device memory or to library-owned pinned host memory (see the flags).
+ * The stream buffer is not referenced after ibp_open returns. *h receives a handle
+ * owned by the library until ibp_close.
+ * Errors: IBP_EINVAL, IBP_ECORRUPT, IBP_ENOMEM, IBP_EHIP.
+ */
+ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint32_t flags,
+                    ibp_handle **h);
+
+/*
+ * ibp_decompress -- decompress rows [first_row, first_row + n_rows) into d_out
+ * (device memory, n_rows * row_bytes bytes, row-major), on `stream`. This is the
+ * drop-in replacement for a host-to-device copy of those rows (Sec. 4.3 and the
+ * Python decompress of the paper's library). With IBP_OPEN_PAYLOAD_HOST the packed
+ * bytes cross PCIe in chunks, each copy overlapping the previous chunk's decode.
+ * Errors: IBP_EINVAL (null handle/output with n_rows > 0), IBP_ERANGE (range outside
+ * the stream), IBP_ENOMEM (out_cap < n_rows * row_bytes), IBP_EHIP, IBP_ESTATE.
+ */
+ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, void *d_out,
+                          uint64_t out_cap, void *stream);
+
+/*
+ * ibp_gather_decompress -- d_out[i] = row(row_ids[i]) for i < n_ids, with row_ids in
+ * host memory (read before the call returns; duplicates allowed) and d_out in device
+ * memory (n_ids * row_bytes bytes). This is the one-call lookup + transfer +
+ * decompress of the paper's embedding integration (Sec. 6.3) and GNN feature
+ * gathering. With IBP_OPEN_PAYLOAD_HOST the host packs the selected packed rows into
+ * pinned staging, which crosses PCIe chunk by chunk overlapped with the decode.
+ * Errors: IBP_EINVAL, IBP_ERANGE (an id out of range; nothing is enqueued),
+ * IBP_ENOMEM (out_cap too small), IBP_EHIP, IBP_ESTATE.
+ */
+ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids,
+                                 void *d_out, uint64_t out_cap, void *stream);
+
+/*
+ * ibp_gather_decompress_device -- as ibp_gather_decompress, with the row ids already
+ * in device memory (d_row_ids, n_ids int64 values), for a handle whose payload is in
+ * device memory (IBP_OPEN_PAYLOAD_DEVICE): every input is resident in HBM and the
+ * call only enqueues the gather kernel. Ids cannot be checked on the host: a row
+ * whose id is out of range is written as zeros and counted in a device-side error
+ * counter that ibp_device_errors() reads.
+ * Errors: IBP_EINVAL (null pointers with n_ids > 0, or a host-payload handle),
+ * IBP_ENOMEM (out_cap too small), IBP_EHIP, IBP_ESTATE.
+ */
+ibp_status ibp_gather_decompress_device(ibp_handle *h, const int64_t *d_row_ids,
+                                        uint64_t n_ids, void *d_out, uint64_t out_cap,
+                                        void *stream);
+
+/*
+ * ibp_device_errors -- synchronize the device and return (in *count) how many
+ * out-of-range device ids the gather kernels met since ibp_open or the last call of
+ * this function, then reset the counter.
+ * Errors: IBP_EINVAL, IBP_EHIP, IBP_ESTATE.
+ */
+ibp_status ibp_device_errors(ibp_handle *h, uint64_t *count);
+
+/* ibp_get_desc / ibp_get_stats -- copies of the handle's description and counters. */
+ibp_status ibp_get_desc(ibp_handle *h, ibp_desc *d);
+ibp_status ibp_get_stats(ibp_handle *h, ibp_stats *st);
+ibp_status ibp_reset_stats(ibp_handle *h);
+
+/*
+ * ibp_close -- wait for the handle's outstanding work, free everything it owns and
+ * invalidate it. NULL is accepted (IBP_OK). Closing twice is undefined: the handle
+ * memory is freed by the first close.
+ */
+ibp_status ibp_close(ibp_handle *h);
+
+/* ibp_last_error -- message of the last failed call on this thread ("" if none). */
+const char *ibp_last_error(void);
+
+/* ibp_version -- library/stream format version string. */
+const char *ibp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IBP_H */

@@ -29,8 +29,9 @@ def _as_rows(rows):
     if a.ndim != 2:
         raise ValueError("rows must be 2-D (n_rows, bytes or elements)")
     n = a.shape[0]
-    b = a.view(np.uint8).reshape(n, -1)
-    return b, n, b.shape[1]
+    L = a.shape[1] * a.itemsize
+    b = a.view(np.uint8).reshape(n, L) if n else np.zeros((0, L), np.uint8)
+    return b, n, L
 
 
 class OracleLib:

@@ -1,0 +1,39 @@
+// Launchers of the gfx950 decompression kernels (ibp_kernels.hip).
+#pragma once
+
+#include <cstdint>
+
+#include <hip/hip_runtime.h>
+
+namespace ibp {
+namespace dev {
+
+// What the kernels need to know about a stream resident on the device.
+struct DevStream {
+    const uint32_t *meta;    // per group: Mask[W] then Bitval[W] (32-bit words)
+    const uint64_t *index;   // off[0..n_groups] (payload byte offsets)
+    uint64_t n_rows;
+    uint64_t n_groups;
+    uint64_t g_magic;        // ceil(2^64 / G) for G >= 2: id / G = mulhi(id, g_magic)
+    uint32_t W;              // 32-bit words per row
+    uint32_t G;              // rows per group
+};
+
+uint64_t div_magic(uint32_t G);
+
+// Rows [first, first + n) into out (row-major). Packed row r of group g is read at byte
+// off[g] - pay_base + (r - g*G) * rb_g of `payload`, which must be readable for 8 bytes
+// past the last packed byte.
+hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_t pay_base,
+                             void *out, uint64_t first, uint64_t n, hipStream_t stream);
+
+// out[i] = row(ids[i]) for i < n. If soff is null, packed rows are read from the
+// device-resident payload at off[g] + r*rb_g; otherwise row i's packed bytes start at
+// byte soff[i] of `payload` (host-packed staging). Ids outside [0, n_rows) give a zero
+// row and one increment of *err.
+hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids,
+                         const uint32_t *soff, uint64_t n, void *out,
+                         unsigned long long *err, hipStream_t stream);
+
+}  // namespace dev
+}  // namespace ibp

@@ -1,0 +1,41 @@
+// Internal declarations shared by the host and device halves of the library.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "ibp.h"
+
+namespace ibp {
+
+constexpr uint32_t kHeaderBytes = 64;
+constexpr uint32_t kVersion = 1;
+constexpr char kMagic[4] = {'I', 'B', 'P', '1'};
+
+// Parsed, validated view of a version-1 stream.
+struct StreamView {
+    const uint8_t *base = nullptr;
+    ibp_desc d{};
+    const uint8_t *meta() const { return base + d.meta_off; }
+    const uint8_t *index_bytes() const { return base + d.index_off; }
+    const uint8_t *payload() const { return base + d.payload_off; }
+    uint64_t off(uint64_t g) const;            // index entry g (unaligned-safe read)
+    uint64_t rows_in_group(uint64_t g) const;
+};
+
+// Thread-local error message plumbing.
+ibp_status fail(ibp_status s, const std::string &msg);
+void clear_error();
+
+// Validate `stream` and fill `v`; on failure sets the error message.
+ibp_status parse_stream(const void *stream, uint64_t stream_bytes, StreamView &v);
+
+// Bytes of one packed row of a group whose Mask has P set bits.
+inline uint64_t packed_row_bytes(uint32_t row_bytes, uint64_t mask_popcount) {
+    return (uint64_t)row_bytes - mask_popcount / 8;
+}
+
+int online_cpus();
+
+}  // namespace ibp

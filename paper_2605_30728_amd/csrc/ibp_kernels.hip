@@ -1,0 +1,426 @@
+// gfx950 decompression kernels of Invariant Bit Packing.
+//
+// The paper decodes one tensor per warp (Sec. 4.3): each thread takes a chunk, counts
+// the unset Mask bits of its chunk, an exclusive scan over the warp gives every chunk's
+// starting bit, and each thread then pulls its bits out of a shared workspace. The
+// kernels here keep that structure, shaped for CDNA4 wave64 and for clusters of rows
+// sharing one Mask/Bitval:
+//
+//   * one wave owns a cluster (decompress) or a segment of requested rows (gather);
+//     lane t owns the 32-bit words t, t+64, t+128, ... of a row, so every output store
+//     of the wave is 64 consecutive dwords (256 B, fully coalesced);
+//   * per cluster, each lane loads Mask/Bitval for its words, counts n_w =
+//     popcount(~Mask_w), and a wave inclusive scan built from DPP row shifts and row
+//     broadcasts turns the counts into bit offsets S_w inside a packed row. Under the
+//     cluster threshold T = cluster size the offsets depend only on the Mask, so they
+//     are computed once per cluster and reused for all of its rows;
+//   * per cluster, each word's variant positions (~Mask_w) are split into runs of
+//     consecutive bits; a run is placed by one funnel rotate (v_alignbit) and one
+//     and-or, so rebuilding a word is: funnel-shift its 32-bit window out of two
+//     packed dwords, then Bitval_w | sum over runs of (rotr(x, r_k) & run_k). Words
+//     with more runs than the register budget take a generic bit-run loop;
+//   * packed rows are byte-aligned and of any length, so a word's window is read as
+//     two dwords at its bit offset and funnel-shifted (v_alignbit_b32), never with
+//     sub-dword loads. No MFMA anywhere: nothing here is a contraction.
+#include "ibp_device.hpp"
+
+namespace ibp {
+namespace dev {
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kWavesPerBlock = 4;
+constexpr int kBlock = kWave * kWavesPerBlock;
+
+__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
+
+// Inclusive prefix sum over the 64 lanes of a wave: row_shr 1/2/4/8 scan each row of
+// 16 lanes, row_bcast:15 carries rows 0->1 and 2->3, row_bcast:31 carries rows 0-1
+// into rows 2-3. Disabled or out-of-row sources contribute 0 (old value 0).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+    int x = (int)v;
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
+    return (uint32_t)x;
+}
+
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(v), 63);
+}
+
+// Per-wave decode state for one tile of a row (64*K words) of one cluster.
+template <int K, int MAXR>
+struct Tile {
+    uint32_t bv[K];          // Bitval of the lane's words
+    uint32_t nm[K];          // ~Mask: the variant positions
+    uint32_t s[K];           // bit offset of the word inside the packed row
+    uint32_t rot[K][MAXR];   // rotate-right amount that lands run k at its position
+    uint32_t rm[K][MAXR];    // run k's bits in place
+    uint32_t bits;           // packed bits of this tile (wave-uniform)
+    int nr;                  // runs applied per word (uniform); -1 = generic loop
+};
+
+template <int K, int MAXR>
+__device__ __forceinline__ void tile_setup(Tile<K, MAXR> &t, const uint32_t *__restrict__ mg,
+                                           uint32_t W, uint32_t w0, uint32_t carry) {
+    const uint32_t l = lane_id();
+    uint32_t c = carry;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const uint32_t w = w0 + l + kWave * j;
+        uint32_t m = 0xFFFFFFFFu, b = 0u;
+        if (w < W) {
+            m = mg[w];
+            b = mg[W + w];
+        }
+        t.nm[j] = ~m;
+        t.bv[j] = b;
+        const uint32_t n = (uint32_t)__builtin_popcount(~m);
+        const uint32_t inc = wave_incl_scan(n);
+        t.s[j] = c + inc - n;
+        c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+    }
+    t.bits = c - carry;
+
+    int cnt_max = 0;
+    bool rest = false;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        uint32_t v = t.nm[j];
+        uint32_t so = 0;
+        int cnt = 0;
+#pragma unroll
+        for (int k = 0; k < MAXR; ++k) {
+            const uint32_t low = v & (0u - v);
+            const uint32_t tt = v + low;      // carries through the lowest run
+            const uint32_t run = v & ~tt;
+            v &= tt;
+            const uint32_t lo = (uint32_t)__builtin_ctz(run | 0x80000000u);
+            t.rot[j][k] = (so - lo) & 31u;
+            t.rm[j][k] = run;
+            so += (uint32_t)__builtin_popcount(run);
+            cnt += run != 0u;
+        }
+        cnt_max = cnt > cnt_max ? cnt : cnt_max;
+        rest = rest || v != 0u;
+    }
+    if (__any(rest)) {
+        t.nr = -1;
+    } else {
+        int nr = 0;
+#pragma unroll
+        for (int k = 0; k < MAXR; ++k)
+            if (__any(cnt_max > k)) nr = k + 1;
+        t.nr = nr;
+    }
+}
+
+// Rebuild one word from its 32-bit window x: Bitval | the NR runs of variant bits.
+template <int NR, int K, int MAXR>
+__device__ __forceinline__ uint32_t word_fast(const Tile<K, MAXR> &t, int j, uint32_t x) {
+    uint32_t acc = t.bv[j];
+#pragma unroll
+    for (int k = 0; k < NR; ++k) acc |= __builtin_amdgcn_alignbit(x, x, t.rot[j][k]) & t.rm[j][k];
+    return acc;
+}
+
+// Generic rebuild for any Mask: walk the runs of ~Mask from the lowest bit up.
+__device__ __forceinline__ uint32_t word_generic(uint32_t bv, uint32_t nm, uint32_t x) {
+    uint32_t acc = bv, v = nm;
+    while (v) {
+        const uint32_t low = v & (0u - v);
+        const uint32_t tt = v + low;
+        const uint32_t run = v & ~tt;
+        v &= tt;
+        acc |= (x << __builtin_ctz(run)) & run;
+        x = __builtin_amdgcn_alignbit(0u, x, (uint32_t)__builtin_popcount(run));
+    }
+    return acc;
+}
+
+// Decode RB rows of one cluster. `at.byte(i)` is the payload byte where row i's packed
+// bits start and `at.out(i)` the row's output; both are wave-uniform. All loads of the
+// batch are issued before any word is rebuilt, so RB*K loads are in flight per wave.
+// NR >= 0 applies NR precomputed runs per word; NR < 0 takes the generic loop.
+template <int NR, int RB, int K, int MAXR, class At>
+__device__ __forceinline__ void decode_batch(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                             const At &at, uint32_t W, uint32_t w0) {
+    const uint32_t l = lane_id();
+    uint32_t d0[RB][K], d1[RB][K], b[RB][K];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+        const uint64_t rbyte = at.byte(i);
+        const uint32_t *__restrict__ p = pay32 + (rbyte >> 2);
+        const uint32_t bit0 = ((uint32_t)rbyte & 3u) * 8u;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            b[i][j] = bit0 + t.s[j];
+            const uint32_t q = b[i][j] >> 5;
+            d0[i][j] = p[q];
+            d1[i][j] = p[q + 1];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+        uint32_t *__restrict__ o = at.out(i);
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t x = __builtin_amdgcn_alignbit(d1[i][j], d0[i][j], b[i][j]);
+            uint32_t v;
+            if constexpr (NR >= 0) v = word_fast<NR>(t, j, x);
+            else v = word_generic(t.bv[j], t.nm[j], x);
+            const uint32_t w = w0 + l + kWave * j;
+            if (w < W) o[w] = v;
+        }
+    }
+}
+
+// Decode rows [0, n) of one cluster with the run count fixed at compile time.
+template <int NR, int K, int MAXR, class At>
+__device__ __forceinline__ void decode_rows_nr(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                               uint32_t n, const At &at, uint32_t W, uint32_t w0) {
+    constexpr int RB = K <= 1 ? 8 : (K <= 2 ? 4 : (K <= 4 ? 2 : 1));
+    uint32_t k = 0;
+    for (; k + RB <= n; k += RB) decode_batch<NR, RB>(t, pay32, at.shifted(k), W, w0);
+    for (; k < n; ++k) decode_batch<NR, 1>(t, pay32, at.shifted(k), W, w0);
+}
+
+template <int K, int MAXR, class At>
+__device__ __forceinline__ void decode_rows(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                            uint32_t n, const At &at, uint32_t W, uint32_t w0) {
+    switch (t.nr) {   // wave-uniform
+    case 0: decode_rows_nr<0>(t, pay32, n, at, W, w0); break;
+    case 1: decode_rows_nr<1>(t, pay32, n, at, W, w0); break;
+    case 2: if constexpr (MAXR >= 2) decode_rows_nr<2>(t, pay32, n, at, W, w0); break;
+    case 3: if constexpr (MAXR >= 3) decode_rows_nr<3>(t, pay32, n, at, W, w0); break;
+    case 4: if constexpr (MAXR >= 4) decode_rows_nr<4>(t, pay32, n, at, W, w0); break;
+    default: decode_rows_nr<-1>(t, pay32, n, at, W, w0); break;
+    }
+}
+
+// Rows of a contiguous slice: row i at byte base + i*rb, output out0 + i*W.
+struct SliceAt {
+    uint64_t base, rb;
+    uint32_t *out0;
+    uint32_t W;
+    __device__ uint64_t byte(int i) const { return base + (uint64_t)i * rb; }
+    __device__ uint32_t *out(int i) const { return out0 + (uint64_t)i * W; }
+    __device__ SliceAt shifted(uint32_t k) const { return {base + k * rb, rb, out0 + (uint64_t)k * W, W}; }
+};
+
+// Rows of a run of gathered ids from one cluster: the row index inside the cluster
+// (or the staged byte offset) of request i0+i sits in lane i0+i of `rloc`.
+struct GatherAt {
+    uint64_t base, rb;       // cluster payload byte and packed row bytes (device payload)
+    uint32_t *seg_out;       // output row of request 0 of the wave's segment
+    uint32_t W;
+    uint32_t i0;             // first request of this run, relative to the segment
+    uint32_t rloc;           // per lane: row inside the cluster, or staged byte offset
+    bool staged;
+    __device__ uint64_t byte(int i) const {
+        const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)rloc, (int)(i0 + i));
+        return staged ? (uint64_t)v : base + (uint64_t)v * rb;
+    }
+    __device__ uint32_t *out(int i) const { return seg_out + (uint64_t)(i0 + i) * W; }
+    __device__ GatherAt shifted(uint32_t k) const {
+        GatherAt a = *this;
+        a.i0 += k;
+        return a;
+    }
+};
+
+// Packed bits of a full row of the cluster whose metadata starts at mg.
+__device__ __forceinline__ uint32_t row_bits(const uint32_t *__restrict__ mg, uint32_t W) {
+    uint32_t n = 0;
+    for (uint32_t w = lane_id(); w < W; w += kWave) n += (uint32_t)__builtin_popcount(~mg[w]);
+    return wave_sum(n);
+}
+
+// Decode n rows of a cluster whose rows span several tiles: tile by tile, each tile's
+// setup carrying the bit offset of the tiles before it.
+template <int K, int MAXR, class At>
+__device__ __forceinline__ void decode_rows_tiled(const uint32_t *__restrict__ mg,
+                                                  const uint32_t *__restrict__ pay32, uint32_t n,
+                                                  const At &at, uint32_t W) {
+    uint32_t carry = 0;
+    for (uint32_t w0 = 0; w0 < W; w0 += kWave * K) {
+        Tile<K, MAXR> t;
+        tile_setup(t, mg, W, w0, carry);
+        decode_rows(t, pay32, n, at, W, w0);
+        carry += t.bits;
+    }
+}
+
+__device__ __forceinline__ uint64_t wave_slot() {
+    return (uint64_t)blockIdx.x * kWavesPerBlock +
+           (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+}
+
+// One wave per unit = (cluster, slice of at most rpu rows of it).
+template <int K, int MAXR>
+__global__ __launch_bounds__(kBlock) void k_decompress(DevStream s, const uint32_t *__restrict__ pay32,
+                                                        uint64_t pay_base, uint32_t *__restrict__ out,
+                                                        uint64_t first, uint64_t n, uint64_t g0,
+                                                        uint64_t n_units, uint32_t upg, uint32_t rpu) {
+    const uint64_t unit = wave_slot();
+    if (unit >= n_units) return;
+    const uint64_t g = g0 + unit / upg;
+    const uint64_t gstart = g * s.G;
+    uint64_t r_lo = gstart + (unit % upg) * (uint64_t)rpu;
+    uint64_t r_hi = min(r_lo + rpu, min(gstart + s.G, s.n_rows));
+    r_lo = max(r_lo, first);
+    r_hi = min(r_hi, first + n);
+    if (r_lo >= r_hi) return;
+    const uint32_t W = s.W;
+    const uint32_t *__restrict__ mg = s.meta + g * 2ull * W;
+    const uint64_t base = s.index[g] - pay_base;
+    const uint32_t rows = (uint32_t)(r_hi - r_lo);
+    if (W <= (uint32_t)(kWave * K)) {
+        Tile<K, MAXR> t;
+        tile_setup(t, mg, W, 0, 0);
+        const uint64_t rb = (t.bits + 7u) >> 3;
+        const SliceAt at{base + (r_lo - gstart) * rb, rb, out + (r_lo - first) * W, W};
+        decode_rows(t, pay32, rows, at, W, 0);
+    } else {
+        const uint64_t rb = (row_bits(mg, W) + 7u) >> 3;
+        const SliceAt at{base + (r_lo - gstart) * rb, rb, out + (r_lo - first) * W, W};
+        decode_rows_tiled<K, MAXR>(mg, pay32, rows, at, W);
+    }
+}
+
+// One wave per segment of up to 64 requests. Lane i loads request i's id; runs of
+// consecutive requests that fall in the same cluster (sorted ids) share one setup.
+template <int K, int MAXR, bool STAGED>
+__global__ __launch_bounds__(kBlock) void k_gather(DevStream s, const uint32_t *__restrict__ pay32,
+                                                    const int64_t *__restrict__ ids,
+                                                    const uint32_t *__restrict__ soff, uint64_t n,
+                                                    uint32_t *__restrict__ out, uint32_t seg,
+                                                    unsigned long long *err) {
+    const uint64_t i0 = wave_slot() * seg;
+    if (i0 >= n) return;
+    const uint32_t cnt = (uint32_t)min((uint64_t)seg, n - i0);
+    const uint32_t l = lane_id();
+    const uint32_t W = s.W;
+    int64_t id = -1;
+    uint32_t so = 0;
+    if (l < cnt) {
+        id = ids[i0 + l];
+        if constexpr (STAGED) so = soff[i0 + l];
+    }
+    const bool valid = l < cnt && id >= 0 && (uint64_t)id < s.n_rows;
+    const uint64_t uid = valid ? (uint64_t)id : 0;
+    const uint64_t g_l = s.G == 1 ? uid : __umul64hi(uid, s.g_magic);
+    const uint32_t r_l = (uint32_t)(uid - g_l * s.G);
+    const uint64_t bad = __ballot(l < cnt && !valid);
+    uint32_t *__restrict__ out_seg = out + i0 * W;
+    if (bad) {
+        // zero the rows of out-of-range ids and count them
+        for (uint32_t i = 0; i < cnt; ++i) {
+            if ((bad >> i) & 1ull) {
+                for (uint32_t w = l; w < W; w += kWave) out_seg[(uint64_t)i * W + w] = 0u;
+            }
+        }
+        if (l == 0) atomicAdd(err, (unsigned long long)__popcll(bad));
+    }
+    const uint32_t g_lo = (uint32_t)g_l, g_hi = (uint32_t)(g_l >> 32);
+    uint32_t i = 0;
+    while (i < cnt) {
+        if ((bad >> i) & 1ull) {
+            ++i;
+            continue;
+        }
+        const uint32_t gl = (uint32_t)__builtin_amdgcn_readlane((int)g_lo, (int)i);
+        const uint32_t gh = (uint32_t)__builtin_amdgcn_readlane((int)g_hi, (int)i);
+        const uint64_t g = ((uint64_t)gh << 32) | gl;
+        // end of the run: first later request in another cluster, invalid, or past cnt
+        const uint64_t other = __ballot(l >= cnt || !valid || g_lo != gl || g_hi != gh);
+        const uint64_t later = other & ~((2ull << i) - 1ull);
+        const uint32_t end = later ? (uint32_t)__builtin_ctzll(later) : cnt;
+        const uint32_t *__restrict__ mg = s.meta + g * 2ull * W;
+        GatherAt at{0, 0, out_seg, W, i, STAGED ? so : r_l, STAGED};
+        if (W <= (uint32_t)(kWave * K)) {
+            Tile<K, MAXR> t;
+            tile_setup(t, mg, W, 0, 0);
+            at.rb = (t.bits + 7u) >> 3;
+            if constexpr (!STAGED) at.base = s.index[g];
+            decode_rows(t, pay32, end - i, at, W, 0);
+        } else {
+            at.rb = (row_bits(mg, W) + 7u) >> 3;
+            if constexpr (!STAGED) at.base = s.index[g];
+            decode_rows_tiled<K, MAXR>(mg, pay32, end - i, at, W);
+        }
+        i = end;
+    }
+}
+
+// Words-per-lane tile shape for a row of W words: (K, MAXR).
+int pick_k(uint32_t W) {
+    if (W <= 64) return 1;
+    if (W <= 128) return 2;
+    if (W <= 256) return 4;
+    return 8;
+}
+
+}  // namespace
+
+uint64_t div_magic(uint32_t G) {
+    if (G <= 1) return 0;
+    // ceil(2^64 / G) = floor((2^64 - 1) / G) + 1 for every G >= 2. With magic =
+    // 2^64/G + e (0 <= e < 1), mulhi(id, magic) = floor(id/G + id*e/2^64) equals
+    // floor(id/G) whenever id * G < 2^64, which ibp_open checks.
+    return ~0ull / G + 1;
+}
+
+hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_t pay_base, void *out,
+                             uint64_t first, uint64_t n, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const uint64_t g0 = first / s.G, g1 = (first + n - 1) / s.G;
+    const uint32_t rpu = s.G <= 64 ? s.G : 64;
+    const uint32_t upg = (s.G + rpu - 1) / rpu;
+    const uint64_t n_units = (g1 - g0 + 1) * upg;
+    const uint64_t blocks = (n_units + kWavesPerBlock - 1) / kWavesPerBlock;
+    const auto *p = reinterpret_cast<const uint32_t *>(payload);
+    auto *o = static_cast<uint32_t *>(out);
+    dim3 grid((unsigned)blocks), block(kBlock);
+    switch (pick_k(s.W)) {
+    case 1: hipLaunchKernelGGL((k_decompress<1, 4>), grid, block, 0, stream, s, p, pay_base, o, first, n, g0, n_units, upg, rpu); break;
+    case 2: hipLaunchKernelGGL((k_decompress<2, 4>), grid, block, 0, stream, s, p, pay_base, o, first, n, g0, n_units, upg, rpu); break;
+    case 4: hipLaunchKernelGGL((k_decompress<4, 2>), grid, block, 0, stream, s, p, pay_base, o, first, n, g0, n_units, upg, rpu); break;
+    default: hipLaunchKernelGGL((k_decompress<8, 1>), grid, block, 0, stream, s, p, pay_base, o, first, n, g0, n_units, upg, rpu); break;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids, const uint32_t *soff,
+                         uint64_t n, void *out, unsigned long long *err, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const uint32_t seg = 16;
+    const uint64_t waves = (n + seg - 1) / seg;
+    const uint64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    const auto *p = reinterpret_cast<const uint32_t *>(payload);
+    auto *o = static_cast<uint32_t *>(out);
+    dim3 grid((unsigned)blocks), block(kBlock);
+#define IBP_GATHER(KK, RR)                                                                              \
+    do {                                                                                                \
+        if (soff)                                                                                       \
+            hipLaunchKernelGGL((k_gather<KK, RR, true>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
+        else                                                                                            \
+            hipLaunchKernelGGL((k_gather<KK, RR, false>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
+    } while (0)
+    switch (pick_k(s.W)) {
+    case 1: IBP_GATHER(1, 4); break;
+    case 2: IBP_GATHER(2, 4); break;
+    case 4: IBP_GATHER(4, 2); break;
+    default: IBP_GATHER(8, 1); break;
+    }
+#undef IBP_GATHER
+    return hipGetLastError();
+}
+
+}  // namespace dev
+}  // namespace ibp

@@ -1,0 +1,570 @@
+// Device runtime of the library: handles, metadata upload, the PCIe staging pipeline
+// and the C ABI entry points that enqueue the decompression kernels.
+//
+// Data layout in device memory (per handle):
+//   d_meta    n_groups * 2 * row_bytes  Mask then Bitval per group, as in the stream
+//   d_index   (n_groups + 1) u64        payload byte offset of every group
+//   d_payload payload_bytes + slack     packed rows (IBP_OPEN_PAYLOAD_DEVICE only)
+// The kernels read a word's 64-bit window as two dwords at its bit offset, so every
+// payload buffer the kernels see (device payload or staging) has kSlack readable bytes
+// past its last packed byte.
+//
+// PCIe path (IBP_OPEN_PAYLOAD_HOST): the packed payload lives in library-owned pinned
+// host memory. Two device staging buffers alternate; for chunk k the side copy stream
+// first waits until the kernel that read buffer k%2 two chunks ago has finished, copies
+// the chunk in, and records an event that the caller's stream waits on before the
+// decode kernel (the paper overlaps CPU memory reads with decoding, Sec. 4.3; here the
+// overlap is between DMA of chunk k+1 and decode of chunk k). For gathers the host first
+// packs the selected packed rows, their ids and staged offsets into pinned staging
+// (multi-threaded), which is the host half of the paper's lookup + transfer.
+#include <algorithm>
+#include <atomic>
+#include <chrono>
+#include <condition_variable>
+#include <cstring>
+#include <functional>
+#include <mutex>
+#include <new>
+#include <thread>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+#include "ibp_device.hpp"
+#include "ibp_internal.hpp"
+
+namespace ibp {
+namespace {
+
+constexpr uint64_t kSlack = 256;                 // readable bytes past any payload end
+constexpr uint64_t kStageBytes = 64ull << 20;    // one staging buffer
+
+uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+// Best-effort calls (cleanup, device restore) whose status is deliberately ignored.
+inline void ignore(hipError_t) {}
+
+// A small persistent worker pool for host packing and large host copies.
+class Pool {
+public:
+    explicit Pool(int n) {
+        for (int i = 0; i < n - 1; ++i) workers_.emplace_back([this] { loop(); });
+    }
+    ~Pool() {
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            stop_ = true;
+            ++gen_;
+        }
+        cv_.notify_all();
+        for (auto &t : workers_) t.join();
+    }
+    int size() const { return (int)workers_.size() + 1; }
+    // Run fn(lo, hi) over [0, n) in blocks of `block` on every worker and the caller.
+    void run(uint64_t n, uint64_t block, const std::function<void(uint64_t, uint64_t)> &fn) {
+        if (n == 0) return;
+        if (workers_.empty() || n <= block) {
+            fn(0, n);
+            return;
+        }
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            fn_ = &fn;
+            n_ = n;
+            block_ = block;
+            next_.store(0);
+            pending_ = (int)workers_.size();
+            ++gen_;
+        }
+        cv_.notify_all();
+        work();
+        std::unique_lock<std::mutex> lk(mu_);
+        done_.wait(lk, [this] { return pending_ == 0; });
+        fn_ = nullptr;
+    }
+
+private:
+    void work() {
+        for (;;) {
+            uint64_t lo = next_.fetch_add(block_);
+            if (lo >= n_) break;
+            (*fn_)(lo, std::min(n_, lo + block_));
+        }
+    }
+    void loop() {
+        uint64_t seen = 0;
+        for (;;) {
+            {
+                std::unique_lock<std::mutex> lk(mu_);
+                cv_.wait(lk, [&] { return gen_ != seen; });
+                seen = gen_;
+                if (stop_) return;
+            }
+            work();
+            {
+                std::lock_guard<std::mutex> g(mu_);
+                if (--pending_ == 0) done_.notify_one();
+            }
+        }
+    }
+    std::vector<std::thread> workers_;
+    std::mutex mu_;
+    std::condition_variable cv_, done_;
+    const std::function<void(uint64_t, uint64_t)> *fn_ = nullptr;
+    uint64_t n_ = 0, block_ = 1, gen_ = 0;
+    std::atomic<uint64_t> next_{0};
+    int pending_ = 0;
+    bool stop_ = false;
+};
+
+}  // namespace
+}  // namespace ibp
+
+using namespace ibp;
+
+struct ibp_handle {
+    int device = 0;
+    uint32_t flags = 0;
+    ibp_desc d{};
+    dev::DevStream ds{};
+    uint32_t *d_meta = nullptr;
+    uint64_t *d_index = nullptr;
+    uint8_t *d_payload = nullptr;
+    unsigned long long *d_err = nullptr;
+    // host ids of gathers over a device payload
+    int64_t *h_ids = nullptr, *d_ids = nullptr;
+    uint64_t ids_cap = 0;
+    hipEvent_t ev_ids = nullptr;
+    bool ids_pending = false;
+    // PCIe path
+    uint8_t *h_payload = nullptr;
+    std::vector<uint64_t> h_off;
+    std::vector<uint32_t> h_rb;
+    uint8_t *h_stage[2] = {nullptr, nullptr};
+    uint8_t *d_stage[2] = {nullptr, nullptr};
+    hipStream_t copy_stream = nullptr;
+    hipEvent_t ev_copied[2] = {nullptr, nullptr};
+    hipEvent_t ev_free[2] = {nullptr, nullptr};
+    bool stage_used[2] = {false, false};
+    int next_stage = 0;
+    Pool *pool = nullptr;
+    std::atomic<int> busy{0};
+    ibp_stats stats{};
+    hipError_t sticky = hipSuccess;
+};
+
+namespace {
+
+// Marks a handle busy for one call and makes its device current for the call.
+class CallScope {
+public:
+    explicit CallScope(ibp_handle *h) : h_(h) {
+        if (!h_) return;
+        int expected = 0;
+        ok_ = h_->busy.compare_exchange_strong(expected, 1);
+        if (ok_) {
+            ignore(hipGetDevice(&prev_));
+            if (prev_ != h_->device) ignore(hipSetDevice(h_->device));
+        }
+    }
+    ~CallScope() {
+        if (!ok_) return;
+        if (prev_ != h_->device) ignore(hipSetDevice(prev_));
+        h_->busy.store(0);
+    }
+    bool ok() const { return ok_; }
+
+private:
+    ibp_handle *h_;
+    bool ok_ = false;
+    int prev_ = -1;
+};
+
+ibp_status hip_fail(ibp_handle *h, hipError_t e, const char *what) {
+    if (h && h->sticky == hipSuccess) h->sticky = e;
+    return fail(IBP_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define IBP_HIP(h, call)                                  \
+    do {                                                  \
+        hipError_t e_ = (call);                           \
+        if (e_ != hipSuccess) return hip_fail(h, e_, #call); \
+    } while (0)
+
+ibp_status check_handle(ibp_handle *h, const CallScope &cs) {
+    if (!h) return fail(IBP_EINVAL, "handle is null");
+    if (!cs.ok()) return fail(IBP_ESTATE, "handle is in use by another thread");
+    if (h->sticky != hipSuccess)
+        return fail(IBP_EHIP, std::string("earlier HIP error on this handle: ") + hipGetErrorString(h->sticky));
+    return IBP_OK;
+}
+
+void free_handle(ibp_handle *h) {
+    if (!h) return;
+    ignore(hipFree(h->d_meta));
+    ignore(hipFree(h->d_index));
+    ignore(hipFree(h->d_payload));
+    ignore(hipFree(h->d_err));
+    ignore(hipFree(h->d_ids));
+    if (h->h_ids) ignore(hipHostFree(h->h_ids));
+    if (h->h_payload) ignore(hipHostFree(h->h_payload));
+    for (int b = 0; b < 2; ++b) {
+        if (h->h_stage[b]) ignore(hipHostFree(h->h_stage[b]));
+        ignore(hipFree(h->d_stage[b]));
+        if (h->ev_copied[b]) ignore(hipEventDestroy(h->ev_copied[b]));
+        if (h->ev_free[b]) ignore(hipEventDestroy(h->ev_free[b]));
+    }
+    if (h->ev_ids) ignore(hipEventDestroy(h->ev_ids));
+    if (h->copy_stream) ignore(hipStreamDestroy(h->copy_stream));
+    delete h->pool;
+    delete h;
+}
+
+// Ensure the pinned + device id buffers of a handle hold n ids.
+ibp_status ensure_ids(ibp_handle *h, uint64_t n) {
+    if (n <= h->ids_cap) return IBP_OK;
+    if (h->ids_pending) {
+        IBP_HIP(h, hipEventSynchronize(h->ev_ids));
+        h->ids_pending = false;
+    }
+    uint64_t cap = std::max<uint64_t>(n, 2 * h->ids_cap);
+    if (h->h_ids) ignore(hipHostFree(h->h_ids));
+    ignore(hipFree(h->d_ids));
+    h->h_ids = nullptr;
+    h->d_ids = nullptr;
+    h->ids_cap = 0;
+    if (hipHostMalloc((void **)&h->h_ids, cap * 8, hipHostMallocDefault) != hipSuccess)
+        return fail(IBP_ENOMEM, "pinned allocation for row ids failed");
+    if (hipMalloc((void **)&h->d_ids, cap * 8) != hipSuccess)
+        return fail(IBP_ENOMEM, "device allocation for row ids failed");
+    h->ids_cap = cap;
+    return IBP_OK;
+}
+
+ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
+    const ibp_desc &d = h->d;
+    if (hipHostMalloc((void **)&h->h_payload, d.payload_bytes + kSlack, hipHostMallocDefault) != hipSuccess)
+        return fail(IBP_ENOMEM, "pinned allocation for the payload failed");
+    const uint8_t *src = v.payload();
+    uint8_t *dst = h->h_payload;
+    h->pool->run(d.payload_bytes, 64ull << 20, [&](uint64_t lo, uint64_t hi) {
+        std::memcpy(dst + lo, src + lo, hi - lo);
+    });
+    std::memset(dst + d.payload_bytes, 0, kSlack);
+    h->h_off.resize(d.n_groups + 1);
+    h->h_rb.resize(d.n_groups);
+    for (uint64_t g = 0; g <= d.n_groups; ++g) h->h_off[g] = v.off(g);
+    for (uint64_t g = 0; g < d.n_groups; ++g)
+        h->h_rb[g] = (uint32_t)((h->h_off[g + 1] - h->h_off[g]) / v.rows_in_group(g));
+    for (int b = 0; b < 2; ++b) {
+        if (hipHostMalloc((void **)&h->h_stage[b], kStageBytes + kSlack, hipHostMallocDefault) != hipSuccess)
+            return fail(IBP_ENOMEM, "pinned allocation for staging failed");
+        if (hipMalloc((void **)&h->d_stage[b], kStageBytes + kSlack) != hipSuccess)
+            return fail(IBP_ENOMEM, "device allocation for staging failed");
+        IBP_HIP(h, hipMemset(h->d_stage[b], 0, kStageBytes + kSlack));
+        IBP_HIP(h, hipEventCreateWithFlags(&h->ev_copied[b], hipEventDisableTiming));
+        IBP_HIP(h, hipEventCreateWithFlags(&h->ev_free[b], hipEventDisableTiming));
+    }
+    IBP_HIP(h, hipStreamCreateWithFlags(&h->copy_stream, hipStreamNonBlocking));
+    return IBP_OK;
+}
+
+// Claim staging buffer b for a new chunk: the previous copy out of its pinned half must
+// have finished (host wait), and the next copy into its device half must wait for the
+// kernel that last read it (device wait on the copy stream).
+ibp_status claim_stage(ibp_handle *h, int b, bool host_side_too) {
+    if (h->stage_used[b]) {
+        if (host_side_too) IBP_HIP(h, hipEventSynchronize(h->ev_copied[b]));
+        IBP_HIP(h, hipStreamWaitEvent(h->copy_stream, h->ev_free[b], 0));
+    }
+    return IBP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint32_t flags, ibp_handle **out) {
+    clear_error();
+    if (!out) return fail(IBP_EINVAL, "handle output is null");
+    *out = nullptr;
+    if (flags != IBP_OPEN_PAYLOAD_DEVICE && flags != IBP_OPEN_PAYLOAD_HOST)
+        return fail(IBP_EINVAL, "unknown open flags");
+    StreamView v;
+    ibp_status st = parse_stream(stream, stream_bytes, v);
+    if (st != IBP_OK) return st;
+    const ibp_desc &d = v.d;
+    if (d.group_rows > 1 && d.n_rows > ~0ull / d.group_rows)
+        return fail(IBP_EINVAL, "n_rows * group_rows must stay below 2^64");
+    if (2ull * d.row_bytes * 8 > 0xFFFFFFFFull) return fail(IBP_EINVAL, "row_bytes too large");
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || device < 0 || device >= count)
+        return fail(IBP_EINVAL, "no such HIP device");
+    int prev = 0;
+    ignore(hipGetDevice(&prev));
+    if (hipSetDevice(device) != hipSuccess) return fail(IBP_EHIP, "hipSetDevice failed");
+
+    ibp_handle *h = new (std::nothrow) ibp_handle();
+    if (!h) {
+        ignore(hipSetDevice(prev));
+        return fail(IBP_ENOMEM, "host allocation failed");
+    }
+    h->device = device;
+    h->flags = flags;
+    h->d = d;
+    h->pool = new Pool(std::min(16, online_cpus()));
+    auto bail = [&](ibp_status s) {
+        free_handle(h);
+        ignore(hipSetDevice(prev));
+        return s;
+    };
+    const uint64_t meta_bytes = d.n_groups * 2ull * d.row_bytes;
+    if (hipMalloc((void **)&h->d_meta, std::max<uint64_t>(meta_bytes, 4)) != hipSuccess ||
+        hipMalloc((void **)&h->d_index, 8 * (d.n_groups + 1)) != hipSuccess ||
+        hipMalloc((void **)&h->d_err, 8) != hipSuccess)
+        return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
+    if (meta_bytes && hipMemcpy(h->d_meta, v.meta(), meta_bytes, hipMemcpyHostToDevice) != hipSuccess)
+        return bail(fail(IBP_EHIP, "metadata upload failed"));
+    if (hipMemcpy(h->d_index, v.index_bytes(), 8 * (d.n_groups + 1), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemset(h->d_err, 0, 8) != hipSuccess)
+        return bail(fail(IBP_EHIP, "index upload failed"));
+    if (flags == IBP_OPEN_PAYLOAD_DEVICE) {
+        const uint64_t bytes = round_up(d.payload_bytes + kSlack, 256);
+        if (hipMalloc((void **)&h->d_payload, bytes) != hipSuccess)
+            return bail(fail(IBP_ENOMEM, "device allocation for the payload failed"));
+        if (hipMemset(h->d_payload + d.payload_bytes, 0, bytes - d.payload_bytes) != hipSuccess ||
+            (d.payload_bytes &&
+             hipMemcpy(h->d_payload, v.payload(), d.payload_bytes, hipMemcpyHostToDevice) != hipSuccess))
+            return bail(fail(IBP_EHIP, "payload upload failed"));
+    } else {
+        st = setup_host_path(h, v);
+        if (st != IBP_OK) return bail(st);
+    }
+    if (hipEventCreateWithFlags(&h->ev_ids, hipEventDisableTiming) != hipSuccess)
+        return bail(fail(IBP_EHIP, "event creation failed"));
+    if (hipDeviceSynchronize() != hipSuccess) return bail(fail(IBP_EHIP, "upload did not complete"));
+    h->ds.meta = h->d_meta;
+    h->ds.index = h->d_index;
+    h->ds.n_rows = d.n_rows;
+    h->ds.n_groups = d.n_groups;
+    h->ds.g_magic = dev::div_magic(d.group_rows);
+    h->ds.W = d.row_bytes / 4;
+    h->ds.G = d.group_rows;
+    ignore(hipSetDevice(prev));
+    *out = h;
+    return IBP_OK;
+}
+
+ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, void *d_out, uint64_t out_cap,
+                          void *stream) {
+    clear_error();
+    CallScope cs(h);
+    ibp_status st = check_handle(h, cs);
+    if (st != IBP_OK) return st;
+    const ibp_desc &d = h->d;
+    if (first_row > d.n_rows || n_rows > d.n_rows - first_row)
+        return fail(IBP_ERANGE, "row range outside the stream");
+    if (n_rows == 0) return IBP_OK;
+    if (!d_out) return fail(IBP_EINVAL, "output is null");
+    if (out_cap / d.row_bytes < n_rows) return fail(IBP_ENOMEM, "output capacity too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const uint64_t L = d.row_bytes, G = d.group_rows;
+    if (h->flags == IBP_OPEN_PAYLOAD_DEVICE) {
+        IBP_HIP(h, dev::launch_decompress(h->ds, h->d_payload, 0, d_out, first_row, n_rows, s));
+    } else {
+        // chunks of whole groups whose packed bytes fit one staging buffer
+        const uint64_t last = first_row + n_rows;
+        uint64_t ga = first_row / G;
+        const uint64_t gend = (last - 1) / G + 1;
+        while (ga < gend) {
+            uint64_t gb = ga + 1;
+            while (gb < gend && h->h_off[gb + 1] - h->h_off[ga] <= kStageBytes) ++gb;
+            const uint64_t bytes = h->h_off[gb] - h->h_off[ga];
+            if (bytes > kStageBytes) return fail(IBP_EINVAL, "a group is larger than the staging buffer");
+            const int b = h->next_stage;
+            h->next_stage ^= 1;
+            st = claim_stage(h, b, false);
+            if (st != IBP_OK) return st;
+            if (bytes)
+                IBP_HIP(h, hipMemcpyAsync(h->d_stage[b], h->h_payload + h->h_off[ga], bytes, hipMemcpyHostToDevice,
+                                          h->copy_stream));
+            IBP_HIP(h, hipEventRecord(h->ev_copied[b], h->copy_stream));
+            IBP_HIP(h, hipStreamWaitEvent(s, h->ev_copied[b], 0));
+            const uint64_t r0 = std::max(first_row, ga * G), r1 = std::min(last, gb * G);
+            IBP_HIP(h, dev::launch_decompress(h->ds, h->d_stage[b], h->h_off[ga],
+                                              static_cast<uint8_t *>(d_out) + (r0 - first_row) * L, r0, r1 - r0, s));
+            IBP_HIP(h, hipEventRecord(h->ev_free[b], s));
+            h->stage_used[b] = true;
+            h->stats.h2d_bytes += bytes;
+            h->stats.h2d_payload_bytes += bytes;
+            ga = gb;
+        }
+    }
+    h->stats.calls += 1;
+    h->stats.rows_out += n_rows;
+    h->stats.out_bytes += n_rows * L;
+    return IBP_OK;
+}
+
+ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, void *d_out,
+                                 uint64_t out_cap, void *stream) {
+    clear_error();
+    CallScope cs(h);
+    ibp_status st = check_handle(h, cs);
+    if (st != IBP_OK) return st;
+    const ibp_desc &d = h->d;
+    if (n_ids == 0) return IBP_OK;
+    if (!row_ids || !d_out) return fail(IBP_EINVAL, "row ids or output is null");
+    if (out_cap / d.row_bytes < n_ids) return fail(IBP_ENOMEM, "output capacity too small");
+    for (uint64_t i = 0; i < n_ids; ++i)
+        if (row_ids[i] < 0 || (uint64_t)row_ids[i] >= d.n_rows)
+            return fail(IBP_ERANGE, "row id " + std::to_string(row_ids[i]) + " at position " + std::to_string(i) +
+                                        " is outside [0, " + std::to_string(d.n_rows) + ")");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const uint64_t L = d.row_bytes, G = d.group_rows;
+    if (h->flags == IBP_OPEN_PAYLOAD_DEVICE) {
+        st = ensure_ids(h, n_ids);
+        if (st != IBP_OK) return st;
+        if (h->ids_pending) IBP_HIP(h, hipEventSynchronize(h->ev_ids));
+        std::memcpy(h->h_ids, row_ids, n_ids * 8);
+        IBP_HIP(h, hipMemcpyAsync(h->d_ids, h->h_ids, n_ids * 8, hipMemcpyHostToDevice, s));
+        IBP_HIP(h, dev::launch_gather(h->ds, h->d_payload, h->d_ids, nullptr, n_ids, d_out, h->d_err, s));
+        IBP_HIP(h, hipEventRecord(h->ev_ids, s));
+        h->ids_pending = true;
+        h->stats.h2d_bytes += n_ids * 8;
+    } else {
+        // Host packing: each chunk's staging holds [ids | staged offsets | packed rows].
+        uint64_t i0 = 0;
+        while (i0 < n_ids) {
+            // rows that fit: 12 bytes of tables + the packed row rounded to 4 bytes
+            uint64_t i1 = i0, used = 0;
+            while (i1 < n_ids) {
+                const uint64_t g = (uint64_t)row_ids[i1] / G;
+                const uint64_t need = 12 + round_up(h->h_rb[g], 4);
+                if (used + need + 8 > kStageBytes) break;
+                used += need;
+                ++i1;
+            }
+            if (i1 == i0) return fail(IBP_EINVAL, "a row is larger than the staging buffer");
+            const uint64_t nc = i1 - i0;
+            const int b = h->next_stage;
+            h->next_stage ^= 1;
+            st = claim_stage(h, b, true);
+            if (st != IBP_OK) return st;
+            auto t0 = std::chrono::steady_clock::now();
+            uint8_t *stg = h->h_stage[b];
+            int64_t *ids = reinterpret_cast<int64_t *>(stg);
+            uint32_t *soff = reinterpret_cast<uint32_t *>(stg + 8 * nc);
+            const uint64_t pay0 = round_up(8 * nc + 4 * nc, 16);
+            uint8_t *pay = stg + pay0;
+            // staged offsets (serial prefix sum), then parallel copies
+            uint64_t o = 0;
+            for (uint64_t k = 0; k < nc; ++k) {
+                const int64_t id = row_ids[i0 + k];
+                ids[k] = id;
+                soff[k] = (uint32_t)o;
+                o += round_up(h->h_rb[(uint64_t)id / G], 4);
+            }
+            const uint64_t total = pay0 + o;
+            h->pool->run(nc, 2048, [&](uint64_t lo, uint64_t hi) {
+                for (uint64_t k = lo; k < hi; ++k) {
+                    const uint64_t id = (uint64_t)ids[k], g = id / G, r = id - g * G;
+                    const uint32_t rb = h->h_rb[g];
+                    std::memcpy(pay + soff[k], h->h_payload + h->h_off[g] + r * rb, rb);
+                }
+            });
+            h->stats.host_pack_ns +=
+                (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0)
+                    .count();
+            IBP_HIP(h, hipMemcpyAsync(h->d_stage[b], stg, total, hipMemcpyHostToDevice, h->copy_stream));
+            IBP_HIP(h, hipEventRecord(h->ev_copied[b], h->copy_stream));
+            IBP_HIP(h, hipStreamWaitEvent(s, h->ev_copied[b], 0));
+            const uint8_t *dst = h->d_stage[b];
+            IBP_HIP(h, dev::launch_gather(h->ds, dst + pay0, reinterpret_cast<const int64_t *>(dst),
+                                          reinterpret_cast<const uint32_t *>(dst + 8 * nc), nc,
+                                          static_cast<uint8_t *>(d_out) + i0 * L, h->d_err, s));
+            IBP_HIP(h, hipEventRecord(h->ev_free[b], s));
+            h->stage_used[b] = true;
+            h->stats.h2d_bytes += total;
+            h->stats.h2d_payload_bytes += o;
+            i0 = i1;
+        }
+    }
+    h->stats.calls += 1;
+    h->stats.rows_out += n_ids;
+    h->stats.out_bytes += n_ids * L;
+    return IBP_OK;
+}
+
+ibp_status ibp_gather_decompress_device(ibp_handle *h, const int64_t *d_row_ids, uint64_t n_ids, void *d_out,
+                                        uint64_t out_cap, void *stream) {
+    clear_error();
+    CallScope cs(h);
+    ibp_status st = check_handle(h, cs);
+    if (st != IBP_OK) return st;
+    if (h->flags != IBP_OPEN_PAYLOAD_DEVICE)
+        return fail(IBP_EINVAL, "device row ids need a handle opened with IBP_OPEN_PAYLOAD_DEVICE");
+    if (n_ids == 0) return IBP_OK;
+    if (!d_row_ids || !d_out) return fail(IBP_EINVAL, "row ids or output is null");
+    if (out_cap / h->d.row_bytes < n_ids) return fail(IBP_ENOMEM, "output capacity too small");
+    IBP_HIP(h, dev::launch_gather(h->ds, h->d_payload, d_row_ids, nullptr, n_ids, d_out, h->d_err,
+                                  static_cast<hipStream_t>(stream)));
+    h->stats.calls += 1;
+    h->stats.rows_out += n_ids;
+    h->stats.out_bytes += n_ids * h->d.row_bytes;
+    return IBP_OK;
+}
+
+ibp_status ibp_device_errors(ibp_handle *h, uint64_t *count) {
+    clear_error();
+    CallScope cs(h);
+    ibp_status st = check_handle(h, cs);
+    if (st != IBP_OK) return st;
+    if (!count) return fail(IBP_EINVAL, "count is null");
+    IBP_HIP(h, hipDeviceSynchronize());
+    unsigned long long c = 0;
+    IBP_HIP(h, hipMemcpy(&c, h->d_err, 8, hipMemcpyDeviceToHost));
+    IBP_HIP(h, hipMemset(h->d_err, 0, 8));
+    IBP_HIP(h, hipDeviceSynchronize());
+    *count = c;
+    return IBP_OK;
+}
+
+ibp_status ibp_get_desc(ibp_handle *h, ibp_desc *d) {
+    clear_error();
+    if (!h || !d) return fail(IBP_EINVAL, "null argument");
+    *d = h->d;
+    return IBP_OK;
+}
+
+ibp_status ibp_get_stats(ibp_handle *h, ibp_stats *st) {
+    clear_error();
+    if (!h || !st) return fail(IBP_EINVAL, "null argument");
+    *st = h->stats;
+    return IBP_OK;
+}
+
+ibp_status ibp_reset_stats(ibp_handle *h) {
+    clear_error();
+    if (!h) return fail(IBP_EINVAL, "null argument");
+    h->stats = ibp_stats{};
+    return IBP_OK;
+}
+
+ibp_status ibp_close(ibp_handle *h) {
+    clear_error();
+    if (!h) return IBP_OK;
+    int expected = 0;
+    if (!h->busy.compare_exchange_strong(expected, 1))
+        return fail(IBP_ESTATE, "handle is in use by another thread");
+    int prev = 0;
+    ignore(hipGetDevice(&prev));
+    ignore(hipSetDevice(h->device));
+    hipError_t e = hipDeviceSynchronize();
+    free_handle(h);
+    ignore(hipSetDevice(prev));
+    if (e != hipSuccess) return fail(IBP_EHIP, std::string("pending work failed: ") + hipGetErrorString(e));
+    return IBP_OK;
+}
+
+}  // extern "C"
