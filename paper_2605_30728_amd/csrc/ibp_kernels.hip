@@ -293,10 +293,11 @@ __global__ __launch_bounds__(kBlock) void k_decompress(DevStream s, const uint32
     }
 }
 
-// One wave per segment of up to 64 requests. Lane i loads request i's id; runs of
-// consecutive requests that fall in the same cluster (sorted ids) share one setup.
+// Gather of rows wider than one tile (W > 512 words). One wave per segment of up to 64
+// requests; lane i loads request i's id; runs of consecutive requests that fall in the
+// same cluster (sorted ids) share one setup, and each row is decoded tile by tile.
 template <int K, int MAXR, bool STAGED>
-__global__ __launch_bounds__(kBlock) void k_gather(DevStream s, const uint32_t *__restrict__ pay32,
+__global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint32_t *__restrict__ pay32,
                                                     const int64_t *__restrict__ ids,
                                                     const uint32_t *__restrict__ soff, uint64_t n,
                                                     uint32_t *__restrict__ out, uint32_t seg,
@@ -358,6 +359,210 @@ __global__ __launch_bounds__(kBlock) void k_gather(DevStream s, const uint32_t *
     }
 }
 
+// Gather of rows that fit one tile (W <= 64*K), built for memory-level parallelism.
+// A wave owns `seg` requests (lane i loads request i's id) and decodes them RB rows at
+// a time, each row independently: its cluster's Mask/Bitval words, a wave scan of
+// popcount(~Mask) for the bit offsets, then its packed windows. The Mask/Bitval loads of
+// batch b+1 are issued before the rebuilt words of batch b are stored, so a wave keeps
+// RB rows of payload loads, RB rows of metadata loads and its stores in flight together
+// (on gfx9 the vector memory counter also counts stores and drains in order, so loads
+// issued after a batch's stores would wait for those stores as well). Rows are rebuilt
+// with the generic run walk: with a setup per row, precomputed runs would cost more than
+// they save.
+template <int K>
+struct RowMeta {
+    uint32_t m[K], b[K];
+};
+
+// Raw Mask/Bitval words of the lane's words of a row. Lanes past the row's end load a
+// valid word (clamped address) and are masked where the words are used, so the loads
+// carry no exec mask and no default value that would force earlier loads to drain.
+template <int K>
+__device__ __forceinline__ void load_row_meta(RowMeta<K> &rm, const uint32_t *__restrict__ mg, uint32_t W) {
+    const uint32_t l = lane_id();
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const uint32_t w = min(l + kWave * j, W - 1);
+        rm.m[j] = mg[w];
+        rm.b[j] = mg[W + w];
+    }
+}
+
+// Maximum over the 64 lanes of a wave (DPP, as the scan), result in every lane's SGPR.
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+    int x = (int)v;
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false));  // row_shr:1
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false));  // row_shr:2
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false));  // row_shr:4
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false));  // row_shr:8
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
+    return (uint32_t)__builtin_amdgcn_readlane(x, 63);
+}
+
+// Deposit by holes. The variant positions nm of a word span [lo, hi]; inside that span
+// the invariant positions form "holes" (runs of invariant bits). Shifting the packed
+// bits x up to lo places them contiguously; opening a gap of the right width at every
+// hole, lowest first (bits at and above the hole move up by its width), puts each bit on
+// its variant position, and Bitval fills the rest. A word with r runs of variant bits
+// has r - 1 holes.
+__device__ __forceinline__ uint32_t run_count(uint32_t v) { return (uint32_t)__builtin_popcount(v & ~(v << 1)); }
+
+// nh is wave-uniform and at least the word's own hole count; extra iterations find no
+// hole (below = all but bit 31, width 0) and leave y as it is.
+__device__ __forceinline__ uint32_t word_deposit(uint32_t bv, uint32_t nm, uint32_t x, uint32_t nh) {
+    const uint32_t lo = (uint32_t)__builtin_ctz(nm | 0x80000000u);
+    // span [lo, hi] (nm = 0 gives garbage that the final select discards)
+    const uint32_t span = (0xFFFFFFFFu >> __builtin_clz(nm | 1u)) & (0xFFFFFFFFu << lo);
+    uint32_t holes = span & ~nm;   // never holds bit 31: the top of the span is variant
+    uint32_t y = x << lo;
+    for (uint32_t k = 0; k < nh; ++k) {
+        const uint32_t pos = (uint32_t)__builtin_ctz(holes | 0x80000000u);
+        const uint32_t t = holes + (1u << pos);      // carries through the lowest hole
+        const uint32_t width = (uint32_t)__builtin_popcount(holes & ~t);
+        holes &= t;
+        const uint32_t below = (1u << pos) - 1u;
+        y = (y & below) | ((y << width) & ~below);
+    }
+    return (nm & y) | (~nm & bv);
+}
+
+// Exclusive bit offsets of the lane's words inside a packed row (word order t + 64*j)
+// and the row's total packed bits. Two strides share one wave scan: every count is at
+// most 32, so every prefix is at most 2048 and fits a 16-bit field.
+template <int K>
+__device__ __forceinline__ uint32_t row_offsets(const uint32_t (&n)[K], uint32_t (&s)[K]) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < K; j += 2) {
+        if (j + 1 < K) {
+            const uint32_t v = n[j] | (n[j + 1] << 16);
+            const uint32_t inc = wave_incl_scan(v);
+            const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+            s[j] = c + (inc & 0xFFFFu) - n[j];
+            c += tot & 0xFFFFu;
+            s[j + 1] = c + (inc >> 16) - n[j + 1];
+            c += tot >> 16;
+        } else {
+            const uint32_t inc = wave_incl_scan(n[j]);
+            s[j] = c + inc - n[j];
+            c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+        }
+    }
+    return c;
+}
+
+// Blocks are dealt to the 8 XCDs round-robin; renumber them so that consecutive
+// logical blocks (neighbouring sorted ids, which share clusters) run on one XCD and
+// share its L2. A bijection on [0, nblocks) for any nblocks.
+__device__ __forceinline__ uint32_t xcd_block(uint32_t b, uint32_t nblocks) {
+    constexpr uint32_t kXcd = 8;
+    const uint32_t xcd = b % kXcd, idx = b / kXcd;
+    const uint32_t per = nblocks / kXcd, extra = nblocks % kXcd;
+    return xcd * per + min(xcd, extra) + idx;
+}
+
+template <int K, int RB, bool STAGED>
+__global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint32_t *__restrict__ pay32,
+                                                         const int64_t *__restrict__ ids,
+                                                         const uint32_t *__restrict__ soff, uint64_t n,
+                                                         uint32_t *__restrict__ out, uint32_t seg,
+                                                         unsigned long long *err) {
+    const uint64_t slot = (uint64_t)xcd_block(blockIdx.x, gridDim.x) * kWavesPerBlock +
+                          (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
+    const uint64_t i0 = slot * seg;
+    if (i0 >= n) return;
+    const uint32_t cnt = (uint32_t)min((uint64_t)seg, n - i0);
+    const uint32_t l = lane_id();
+    const uint32_t W = s.W;
+    int64_t id = -1;
+    uint32_t so = 0;
+    if (l < cnt) {
+        id = ids[i0 + l];
+        if constexpr (STAGED) so = soff[i0 + l];
+    }
+    const bool valid = l < cnt && id >= 0 && (uint64_t)id < s.n_rows;
+    const uint64_t uid = valid ? (uint64_t)id : 0;
+    const uint64_t g_l = s.G == 1 ? uid : __umul64hi(uid, s.g_magic);
+    const uint32_t r_l = (uint32_t)(uid - g_l * s.G);
+    const uint32_t g_lo = (uint32_t)g_l, g_hi = (uint32_t)(g_l >> 32);
+    // each lane fetches its request's cluster offset once, so rows never wait on an
+    // index load of their own
+    uint64_t off_l = 0;
+    if constexpr (!STAGED) off_l = s.index[g_l];
+    const uint32_t off_lo = (uint32_t)off_l, off_hi = (uint32_t)(off_l >> 32);
+    const uint64_t bad = __ballot(l < cnt && !valid);
+    uint32_t *__restrict__ out_seg = out + i0 * W;
+    if (bad) {
+        for (uint32_t i = 0; i < cnt; ++i)
+            if ((bad >> i) & 1ull)
+                for (uint32_t w = l; w < W; w += kWave) out_seg[(uint64_t)i * W + w] = 0u;
+        if (l == 0) atomicAdd(err, (unsigned long long)__popcll(bad));
+    }
+    auto rd64 = [](uint32_t lo, uint32_t hi, uint32_t i) -> uint64_t {
+        return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)hi, (int)i) << 32) |
+               (uint32_t)__builtin_amdgcn_readlane((int)lo, (int)i);
+    };
+    // request slot i of the segment; slots past the end repeat the last request (their
+    // loads stay in bounds and their stores are skipped)
+    auto slot_of = [&](uint32_t i) { return i < cnt ? i : cnt - 1; };
+    const uint32_t nb = (cnt + RB - 1) / RB;
+    for (uint32_t bb = 0; bb < nb; ++bb) {
+        const uint32_t base_i = bb * RB;
+        RowMeta<K> meta[RB];
+#pragma unroll
+        for (int u = 0; u < RB; ++u)
+            load_row_meta<K>(meta[u], s.meta + rd64(g_lo, g_hi, slot_of(base_i + u)) * 2ull * W, W);
+        uint32_t nm[RB][K], bv[RB][K], d0[RB][K], d1[RB][K], bit[RB][K], nh[RB];
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
+            const uint32_t i = slot_of(base_i + u);
+            uint32_t cntw[K], runs = 0;
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+                const bool in_row = l + kWave * j < W;
+                nm[u][j] = in_row ? ~meta[u].m[j] : 0u;
+                bv[u][j] = in_row ? meta[u].b[j] : 0u;
+                cntw[j] = (uint32_t)__builtin_popcount(nm[u][j]);
+                runs = max(runs, run_count(nm[u][j]));
+            }
+            const uint32_t c = row_offsets<K>(cntw, bit[u]);
+            const uint32_t max_runs = wave_max(runs);
+            nh[u] = max_runs ? max_runs - 1u : 0u;
+            const uint64_t rb = (c + 7u) >> 3;
+            uint64_t rbyte;
+            if constexpr (STAGED) rbyte = (uint32_t)__builtin_amdgcn_readlane((int)so, (int)i);
+            else rbyte = rd64(off_lo, off_hi, i) + (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)r_l, (int)i) * rb;
+            const uint32_t *__restrict__ p = pay32 + (rbyte >> 2);
+            const uint32_t bit0 = ((uint32_t)rbyte & 3u) * 8u;
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+                bit[u][j] += bit0;
+                const uint32_t q = bit[u][j] >> 5;
+                d0[u][j] = p[q];
+                d1[u][j] = p[q + 1];
+            }
+        }
+        uint32_t x[RB][K];
+#pragma unroll
+        for (int u = 0; u < RB; ++u)
+#pragma unroll
+            for (int j = 0; j < K; ++j) x[u][j] = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], bit[u][j]);
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
+            const uint32_t i = base_i + u;
+            const bool row_ok = i < cnt && !((bad >> (i & 63)) & 1ull);
+            uint32_t *__restrict__ orow = out_seg + (uint64_t)slot_of(i) * W;
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+                const uint32_t v = word_deposit(bv[u][j], nm[u][j], x[u][j], nh[u]);
+                const uint32_t w = l + kWave * j;
+                if (row_ok && w < W) orow[w] = v;
+            }
+        }
+    }
+}
+
 // Words-per-lane tile shape for a row of W words: (K, MAXR).
 int pick_k(uint32_t W) {
     if (W <= 64) return 1;
@@ -399,26 +604,41 @@ hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_
 hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids, const uint32_t *soff,
                          uint64_t n, void *out, unsigned long long *err, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    const uint32_t seg = 16;
-    const uint64_t waves = (n + seg - 1) / seg;
-    const uint64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
     const auto *p = reinterpret_cast<const uint32_t *>(payload);
     auto *o = static_cast<uint32_t *>(out);
-    dim3 grid((unsigned)blocks), block(kBlock);
-#define IBP_GATHER(KK, RR)                                                                              \
-    do {                                                                                                \
-        if (soff)                                                                                       \
-            hipLaunchKernelGGL((k_gather<KK, RR, true>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
-        else                                                                                            \
-            hipLaunchKernelGGL((k_gather<KK, RR, false>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
-    } while (0)
-    switch (pick_k(s.W)) {
-    case 1: IBP_GATHER(1, 4); break;
-    case 2: IBP_GATHER(2, 4); break;
-    case 4: IBP_GATHER(4, 2); break;
-    default: IBP_GATHER(8, 1); break;
+    const int k = pick_k(s.W);
+    if (s.W > 512) {
+        const uint32_t seg = 16;
+        const uint64_t blocks = ((n + seg - 1) / seg + kWavesPerBlock - 1) / kWavesPerBlock;
+        if (soff)
+            hipLaunchKernelGGL((k_gather_tiled<8, 1, true>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, s, p,
+                               ids, soff, n, o, seg, err);
+        else
+            hipLaunchKernelGGL((k_gather_tiled<8, 1, false>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, s, p,
+                               ids, soff, n, o, seg, err);
+        return hipGetLastError();
     }
-#undef IBP_GATHER
+    // One batch of RB rows per wave (measured best on the 2.4M x 100 fp32 minibatch:
+    // RB = 4 at K = 2 keeps 58 VGPRs, 8 waves per SIMD; larger batches cost occupancy,
+    // smaller ones memory-level parallelism).
+    const int rb_sel = k == 1 ? 8 : (k == 2 ? 4 : (k == 4 ? 2 : 1));
+    const uint32_t seg = (uint32_t)rb_sel;
+    const uint64_t blocks = ((n + seg - 1) / seg + kWavesPerBlock - 1) / kWavesPerBlock;
+    dim3 grid((unsigned)blocks), block(kBlock);
+#define IBP_GATHER_ROWS(KK, RB)                                                                             \
+    do {                                                                                                    \
+        if (soff)                                                                                           \
+            hipLaunchKernelGGL((k_gather_rows<KK, RB, true>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
+        else                                                                                                \
+            hipLaunchKernelGGL((k_gather_rows<KK, RB, false>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
+    } while (0)
+    switch (k) {
+    case 1: IBP_GATHER_ROWS(1, 8); break;
+    case 2: IBP_GATHER_ROWS(2, 4); break;
+    case 4: IBP_GATHER_ROWS(4, 2); break;
+    default: IBP_GATHER_ROWS(8, 1); break;
+    }
+#undef IBP_GATHER_ROWS
     return hipGetLastError();
 }
 
