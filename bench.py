@@ -14,9 +14,10 @@ Also reported on the same JSON line:
                 its average duration from HIP events, against 8 TB/s;
   cpu_baseline  the CPU oracle (single thread, bit-serial) decoding a bounded sample of
                 one minibatch, in the same unit;
-  e2e           the PCIe path: payload in pinned host memory, host ids, host packing and
-                double-buffered DMA overlapped with decode; effective output GB/s next to
-                raw pinned H2D GB/s and the compression ratio of the bytes moved.
+  e2e           the PCIe-inclusive paths (payload in pinned host memory): the same gather
+                with host packing + staged DMA and with GPU-initiated zero-copy reads, and
+                8 layers of the bf16 KV workload streamed both ways; effective output GB/s
+                next to raw pinned H2D GB/s and the compression ratio of the bytes needed.
 """
 import argparse
 import hashlib
@@ -94,6 +95,67 @@ def raw_h2d_gbs(torch, nbytes, reps=5):
     e.record()
     torch.cuda.synchronize()
     return nbytes * reps / (s.elapsed_time(e) * 1e-3) / 1e9
+
+
+def pcie_legs(torch, ibp, stream, rows, timed, warm, L, G, rb_of_group):
+    """The PCIe-inclusive legs (never `value`): the same minibatch gather with the payload
+    in pinned host memory, (a) host-packed rows through rotating staging + DMA and
+    (b) GPU-initiated zero-copy reads by the gather kernel; and (c) streaming the layers
+    of the bf16 KV workload through ibp_decompress both ways. Effective GB/s = output bytes
+    / wall time; compared with raw pinned H2D and the ratio of output bytes to the packed
+    bytes the path needs (packed rows + 8 B of per-row tables for gathers)."""
+    from workloads import CONFIGS, gen_rows
+    raw = raw_h2d_gbs(torch, 1 << 30)
+    out = torch.empty(max(b.size for b in timed + warm) * L, dtype=torch.uint8, device="cuda")
+    packed = sum(int(rb_of_group[b // G].sum()) + 8 * b.size for b in timed)
+    out_total = sum(b.size * L for b in timed)
+    cr = out_total / packed
+    res = {"raw_h2d_GBps_1GiB": round(raw, 2), "steps": len(timed)}
+    for mode, flags in (("gather_host_pack", ibp.IBP_OPEN_PAYLOAD_HOST),
+                        ("gather_zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)):
+        h = ibp.ibp_open(stream, 0, flags)
+        for b in warm:
+            ibp.ibp_gather_decompress(h, b, out)
+        torch.cuda.synchronize()
+        ibp.ibp_reset_stats(h)
+        t = time.perf_counter()
+        for b in timed:
+            ibp.ibp_gather_decompress(h, b, out)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t
+        st = ibp.ibp_get_stats(h)
+        got = out[:timed[-1].size * L].cpu().numpy().reshape(-1, L)
+        assert np.array_equal(got, rows[timed[-1]]), mode
+        ibp.ibp_close(h)
+        eff = out_total / dt / 1e9
+        res[mode] = {"effective_GBps": round(eff, 2), "cr": round(cr, 3),
+                     "effective_over_cr_raw": round(eff / (cr * raw), 3),
+                     "host_pack_ms_per_batch": round(st["host_pack_ns"] / len(timed) / 1e6, 3)}
+        log(f"[bench] e2e {mode}: {eff:.1f} GB/s effective ({eff / (cr * raw):.2f} of CR x raw)")
+    kv = CONFIGS["kv_bf16"]
+    n = kv.extra["rows_per_layer"]
+    layers = 8
+    krows = gen_rows(kv, 0, layers * n)
+    ks = ibp.ibp_compress(krows, kv.group_rows)
+    kcr = layers * n * kv.row_bytes / ibp.ibp_describe(ks)["payload_bytes"]
+    kout = torch.empty(n * kv.row_bytes, dtype=torch.uint8, device="cuda")
+    for mode, flags in (("kv_stream_staged_dma", ibp.IBP_OPEN_PAYLOAD_HOST),
+                        ("kv_stream_zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)):
+        h = ibp.ibp_open(ks, 0, flags)
+        ibp.ibp_decompress(h, 0, n, kout)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for layer in range(layers):
+            ibp.ibp_decompress(h, layer * n, n, kout)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t
+        assert np.array_equal(kout.cpu().numpy().reshape(-1, kv.row_bytes), krows[(layers - 1) * n:]), mode
+        ibp.ibp_close(h)
+        eff = layers * n * kv.row_bytes / dt / 1e9
+        res[mode] = {"effective_GBps": round(eff, 2), "cr": round(kcr, 3),
+                     "effective_over_cr_raw": round(eff / (kcr * raw), 3), "layers": layers}
+        log(f"[bench] e2e {mode}: {eff:.1f} GB/s effective ({eff / (kcr * raw):.2f} of CR x raw)")
+    return res
 
 
 def main():
@@ -194,31 +256,8 @@ def main():
 
     e2e = None
     if not args.no_e2e:
-        h2 = ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_HOST)
-        ke = min(args.e2e_steps, K)
-        for b in range(3):
-            ibp.ibp_gather_decompress(h2, batches[b], out)
-        torch.cuda.synchronize()
-        ibp.ibp_reset_stats(h2)
-        t = time.perf_counter()
-        for k in range(ke):
-            ibp.ibp_gather_decompress(h2, batches[Wm + k], out)
-        torch.cuda.synchronize()
-        e2e_s = time.perf_counter() - t
-        st = ibp.ibp_get_stats(h2)
-        got = out[:batches[Wm + ke - 1].size * L].cpu().numpy().reshape(-1, L)
-        assert np.array_equal(got, rows[batches[Wm + ke - 1]])
-        ibp.ibp_close(h2)
-        eff = st["out_bytes"] / e2e_s / 1e9
-        per_batch_h2d = st["h2d_bytes"] // ke
-        raw_1g = raw_h2d_gbs(torch, 1 << 30)
-        raw_b = raw_h2d_gbs(torch, int(per_batch_h2d))
-        cr = st["out_bytes"] / st["h2d_bytes"]
-        e2e = {"effective_GBps": round(eff, 2), "raw_h2d_GBps_1GiB": round(raw_1g, 2),
-               "raw_h2d_GBps_batch": round(raw_b, 2), "cr_e2e": round(cr, 3),
-               "effective_over_cr_raw": round(eff / (cr * raw_1g), 3),
-               "host_pack_ms_per_batch": round(st["host_pack_ns"] / ke / 1e6, 3), "steps": ke}
-        log(f"[bench] e2e PCIe path: {eff:.1f} GB/s effective, raw H2D {raw_1g:.1f} GB/s, CR {cr:.2f}")
+        e2e = pcie_legs(torch, ibp, stream, rows, batches[Wm:Wm + args.e2e_steps], batches[:3], L, G,
+                        rb_of_group)
     ibp.ibp_close(h)
 
     line = {

@@ -81,9 +81,14 @@ typedef struct {
 /* Open flags: where the packed payload lives after ibp_open. */
 enum {
     IBP_OPEN_PAYLOAD_DEVICE = 0, /* copied to device memory (HBM) once, at open */
-    IBP_OPEN_PAYLOAD_HOST = 1    /* kept in library-owned pinned host memory; every call
+    IBP_OPEN_PAYLOAD_HOST = 1,   /* kept in library-owned pinned host memory; every call
                                     moves the needed packed bytes over PCIe through
-                                    double-buffered staging on a side stream */
+                                    rotating staging buffers on a side stream (the host
+                                    packs the rows of a gather) */
+    IBP_OPEN_PAYLOAD_HOST_ZERO_COPY = 2 /* kept in library-owned pinned host memory and read
+                                    by the decode kernels themselves over PCIe
+                                    (GPU-initiated transfers, Sec. 4.4): no host packing,
+                                    no staging copies */
 };
 
 /*
@@ -159,11 +164,13 @@ ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t
 /*
  * ibp_gather_decompress_device -- as ibp_gather_decompress, with the row ids already
  * in device memory (d_row_ids, n_ids int64 values), for a handle whose payload is in
- * device memory (IBP_OPEN_PAYLOAD_DEVICE): every input is resident in HBM and the
- * call only enqueues the gather kernel. Ids cannot be checked on the host: a row
+ * device memory (IBP_OPEN_PAYLOAD_DEVICE: every input is resident in HBM and the call
+ * only enqueues the gather kernel) or read in place from pinned host memory
+ * (IBP_OPEN_PAYLOAD_HOST_ZERO_COPY). Ids cannot be checked on the host: a row
  * whose id is out of range is written as zeros and counted in a device-side error
  * counter that ibp_device_errors() reads.
- * Errors: IBP_EINVAL (null pointers with n_ids > 0, or a host-payload handle),
+ * Errors: IBP_EINVAL (null pointers with n_ids > 0, or a handle opened with
+ * IBP_OPEN_PAYLOAD_HOST),
  * IBP_ENOMEM (out_cap too small), IBP_EHIP, IBP_ESTATE.
  */
 ibp_status ibp_gather_decompress_device(ibp_handle *h, const int64_t *d_row_ids,

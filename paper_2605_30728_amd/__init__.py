@@ -22,6 +22,7 @@ STATUS_NAMES = {0: "IBP_OK", 1: "IBP_EINVAL", 2: "IBP_ERANGE", 3: "IBP_ENOMEM", 
                 5: "IBP_EHIP", 6: "IBP_ESTATE"}
 IBP_OPEN_PAYLOAD_DEVICE = 0
 IBP_OPEN_PAYLOAD_HOST = 1
+IBP_OPEN_PAYLOAD_HOST_ZERO_COPY = 2
 
 
 class IbpError(RuntimeError):

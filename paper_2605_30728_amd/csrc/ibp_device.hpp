@@ -27,12 +27,13 @@ uint64_t div_magic(uint32_t G);
 hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_t pay_base,
                              void *out, uint64_t first, uint64_t n, hipStream_t stream);
 
-// out[i] = row(ids[i]) for i < n. If soff is null, packed rows are read from the
-// device-resident payload at off[g] + r*rb_g; otherwise row i's packed bytes start at
-// byte soff[i] of `payload` (host-packed staging). Ids outside [0, n_rows) give a zero
-// row and one increment of *err.
+// out[i] = row i of n requests. Device payload (sg == soff == null): request i is row
+// ids[i], read at off[g] + r*rb_g of the device-resident payload; ids outside
+// [0, n_rows) give a zero row and one increment of *err. Host-packed staging (ids null):
+// request i belongs to cluster sg[i] (validated on the host) and its packed bytes start
+// at byte soff[i] of `payload`. Either payload is readable 8 bytes past its last byte.
 hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids,
-                         const uint32_t *soff, uint64_t n, void *out,
+                         const uint32_t *sg, const uint32_t *soff, uint64_t n, void *out,
                          unsigned long long *err, hipStream_t stream);
 
 }  // namespace dev

@@ -299,6 +299,7 @@ __global__ __launch_bounds__(kBlock) void k_decompress(DevStream s, const uint32
 template <int K, int MAXR, bool STAGED>
 __global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint32_t *__restrict__ pay32,
                                                     const int64_t *__restrict__ ids,
+                                                    const uint32_t *__restrict__ sg,
                                                     const uint32_t *__restrict__ soff, uint64_t n,
                                                     uint32_t *__restrict__ out, uint32_t seg,
                                                     unsigned long long *err) {
@@ -307,16 +308,20 @@ __global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint
     const uint32_t cnt = (uint32_t)min((uint64_t)seg, n - i0);
     const uint32_t l = lane_id();
     const uint32_t W = s.W;
-    int64_t id = -1;
-    uint32_t so = 0;
-    if (l < cnt) {
-        id = ids[i0 + l];
-        if constexpr (STAGED) so = soff[i0 + l];
+    bool valid;
+    uint64_t g_l;
+    uint32_t r_l = 0, so = 0;
+    if constexpr (STAGED) {
+        valid = l < cnt;
+        g_l = valid ? sg[i0 + l] : 0u;
+        so = valid ? soff[i0 + l] : 0u;
+    } else {
+        const int64_t id = l < cnt ? ids[i0 + l] : -1;
+        valid = l < cnt && id >= 0 && (uint64_t)id < s.n_rows;
+        const uint64_t uid = valid ? (uint64_t)id : 0;
+        g_l = s.G == 1 ? uid : __umul64hi(uid, s.g_magic);
+        r_l = (uint32_t)(uid - g_l * s.G);
     }
-    const bool valid = l < cnt && id >= 0 && (uint64_t)id < s.n_rows;
-    const uint64_t uid = valid ? (uint64_t)id : 0;
-    const uint64_t g_l = s.G == 1 ? uid : __umul64hi(uid, s.g_magic);
-    const uint32_t r_l = (uint32_t)(uid - g_l * s.G);
     const uint64_t bad = __ballot(l < cnt && !valid);
     uint32_t *__restrict__ out_seg = out + i0 * W;
     if (bad) {
@@ -465,6 +470,7 @@ __device__ __forceinline__ uint32_t xcd_block(uint32_t b, uint32_t nblocks) {
 template <int K, int RB, bool STAGED>
 __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint32_t *__restrict__ pay32,
                                                          const int64_t *__restrict__ ids,
+                                                         const uint32_t *__restrict__ sg,
                                                          const uint32_t *__restrict__ soff, uint64_t n,
                                                          uint32_t *__restrict__ out, uint32_t seg,
                                                          unsigned long long *err) {
@@ -475,16 +481,22 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
     const uint32_t cnt = (uint32_t)min((uint64_t)seg, n - i0);
     const uint32_t l = lane_id();
     const uint32_t W = s.W;
-    int64_t id = -1;
-    uint32_t so = 0;
-    if (l < cnt) {
-        id = ids[i0 + l];
-        if constexpr (STAGED) so = soff[i0 + l];
+    // lane l < cnt holds request l: its cluster g_l and row r_l inside the cluster (or,
+    // for staged rows, the byte offset `so` of its packed bits)
+    bool valid;
+    uint64_t g_l;
+    uint32_t r_l = 0, so = 0;
+    if constexpr (STAGED) {
+        valid = l < cnt;
+        g_l = valid ? sg[i0 + l] : 0u;
+        so = valid ? soff[i0 + l] : 0u;
+    } else {
+        const int64_t id = l < cnt ? ids[i0 + l] : -1;
+        valid = l < cnt && id >= 0 && (uint64_t)id < s.n_rows;
+        const uint64_t uid = valid ? (uint64_t)id : 0;
+        g_l = s.G == 1 ? uid : __umul64hi(uid, s.g_magic);
+        r_l = (uint32_t)(uid - g_l * s.G);
     }
-    const bool valid = l < cnt && id >= 0 && (uint64_t)id < s.n_rows;
-    const uint64_t uid = valid ? (uint64_t)id : 0;
-    const uint64_t g_l = s.G == 1 ? uid : __umul64hi(uid, s.g_magic);
-    const uint32_t r_l = (uint32_t)(uid - g_l * s.G);
     const uint32_t g_lo = (uint32_t)g_l, g_hi = (uint32_t)(g_l >> 32);
     // each lane fetches its request's cluster offset once, so rows never wait on an
     // index load of their own
@@ -601,8 +613,8 @@ hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_
     return hipGetLastError();
 }
 
-hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids, const uint32_t *soff,
-                         uint64_t n, void *out, unsigned long long *err, hipStream_t stream) {
+hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids, const uint32_t *sg,
+                         const uint32_t *soff, uint64_t n, void *out, unsigned long long *err, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     const auto *p = reinterpret_cast<const uint32_t *>(payload);
     auto *o = static_cast<uint32_t *>(out);
@@ -612,10 +624,10 @@ hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64
         const uint64_t blocks = ((n + seg - 1) / seg + kWavesPerBlock - 1) / kWavesPerBlock;
         if (soff)
             hipLaunchKernelGGL((k_gather_tiled<8, 1, true>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, s, p,
-                               ids, soff, n, o, seg, err);
+                               ids, sg, soff, n, o, seg, err);
         else
             hipLaunchKernelGGL((k_gather_tiled<8, 1, false>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, s, p,
-                               ids, soff, n, o, seg, err);
+                               ids, sg, soff, n, o, seg, err);
         return hipGetLastError();
     }
     // One batch of RB rows per wave (measured best on the 2.4M x 100 fp32 minibatch:
@@ -628,9 +640,9 @@ hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64
 #define IBP_GATHER_ROWS(KK, RB)                                                                             \
     do {                                                                                                    \
         if (soff)                                                                                           \
-            hipLaunchKernelGGL((k_gather_rows<KK, RB, true>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
+            hipLaunchKernelGGL((k_gather_rows<KK, RB, true>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err); \
         else                                                                                                \
-            hipLaunchKernelGGL((k_gather_rows<KK, RB, false>), grid, block, 0, stream, s, p, ids, soff, n, o, seg, err); \
+            hipLaunchKernelGGL((k_gather_rows<KK, RB, false>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err); \
     } while (0)
     switch (k) {
     case 1: IBP_GATHER_ROWS(1, 8); break;

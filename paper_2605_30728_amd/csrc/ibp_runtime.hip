@@ -4,7 +4,9 @@
 // Data layout in device memory (per handle):
 //   d_meta    n_groups * 2 * row_bytes  Mask then Bitval per group, as in the stream
 //   d_index   (n_groups + 1) u64        payload byte offset of every group
-//   d_payload payload_bytes + slack     packed rows (IBP_OPEN_PAYLOAD_DEVICE only)
+//   d_payload payload_bytes + slack     packed rows (IBP_OPEN_PAYLOAD_DEVICE only; with
+//                                       IBP_OPEN_PAYLOAD_HOST_ZERO_COPY the kernels read
+//                                       the pinned host copy through its device address)
 // The kernels read a word's 64-bit window as two dwords at its bit offset, so every
 // payload buffer the kernels see (device payload or staging) has kSlack readable bytes
 // past its last packed byte.
@@ -37,7 +39,8 @@ namespace ibp {
 namespace {
 
 constexpr uint64_t kSlack = 256;                 // readable bytes past any payload end
-constexpr uint64_t kStageBytes = 64ull << 20;    // one staging buffer
+constexpr uint64_t kStageBytes = 16ull << 20;    // one staging buffer
+constexpr int kStages = 3;                        // staging buffers in rotation
 
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
@@ -130,6 +133,7 @@ struct ibp_handle {
     uint32_t *d_meta = nullptr;
     uint64_t *d_index = nullptr;
     uint8_t *d_payload = nullptr;
+    const uint8_t *k_payload = nullptr;   // what the kernels read: d_payload or the pinned host payload
     unsigned long long *d_err = nullptr;
     // host ids of gathers over a device payload
     int64_t *h_ids = nullptr, *d_ids = nullptr;
@@ -140,13 +144,16 @@ struct ibp_handle {
     uint8_t *h_payload = nullptr;
     std::vector<uint64_t> h_off;
     std::vector<uint32_t> h_rb;
-    uint8_t *h_stage[2] = {nullptr, nullptr};
-    uint8_t *d_stage[2] = {nullptr, nullptr};
+    uint32_t max_rb = 0;            // largest packed row of any cluster
+    uint8_t *h_stage[kStages] = {};
+    uint8_t *d_stage[kStages] = {};
     hipStream_t copy_stream = nullptr;
-    hipEvent_t ev_copied[2] = {nullptr, nullptr};
-    hipEvent_t ev_free[2] = {nullptr, nullptr};
-    bool stage_used[2] = {false, false};
+    hipEvent_t ev_copied[kStages] = {};
+    hipEvent_t ev_free[kStages] = {};
+    bool stage_used[kStages] = {};
     int next_stage = 0;
+    std::vector<uint32_t> req_g, req_rb;   // per-request cluster and packed size (host gathers)
+    std::vector<uint64_t> blk_off;         // per-block staged byte offsets (host gathers)
     Pool *pool = nullptr;
     std::atomic<int> busy{0};
     ibp_stats stats{};
@@ -208,7 +215,7 @@ void free_handle(ibp_handle *h) {
     ignore(hipFree(h->d_ids));
     if (h->h_ids) ignore(hipHostFree(h->h_ids));
     if (h->h_payload) ignore(hipHostFree(h->h_payload));
-    for (int b = 0; b < 2; ++b) {
+    for (int b = 0; b < kStages; ++b) {
         if (h->h_stage[b]) ignore(hipHostFree(h->h_stage[b]));
         ignore(hipFree(h->d_stage[b]));
         if (h->ev_copied[b]) ignore(hipEventDestroy(h->ev_copied[b]));
@@ -254,9 +261,13 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
     h->h_off.resize(d.n_groups + 1);
     h->h_rb.resize(d.n_groups);
     for (uint64_t g = 0; g <= d.n_groups; ++g) h->h_off[g] = v.off(g);
-    for (uint64_t g = 0; g < d.n_groups; ++g)
+    for (uint64_t g = 0; g < d.n_groups; ++g) {
         h->h_rb[g] = (uint32_t)((h->h_off[g + 1] - h->h_off[g]) / v.rows_in_group(g));
-    for (int b = 0; b < 2; ++b) {
+        h->max_rb = std::max(h->max_rb, h->h_rb[g]);
+    }
+    if (h->flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) return IBP_OK;   // no staging: kernels read in place
+    if (d.n_groups > 0xFFFFFFFFull) return fail(IBP_EINVAL, "too many clusters for the PCIe path");
+    for (int b = 0; b < kStages; ++b) {
         if (hipHostMalloc((void **)&h->h_stage[b], kStageBytes + kSlack, hipHostMallocDefault) != hipSuccess)
             return fail(IBP_ENOMEM, "pinned allocation for staging failed");
         if (hipMalloc((void **)&h->d_stage[b], kStageBytes + kSlack) != hipSuccess)
@@ -280,6 +291,99 @@ ibp_status claim_stage(ibp_handle *h, int b, bool host_side_too) {
     return IBP_OK;
 }
 
+// PCIe gather: the host packs the requested packed rows into pinned staging chunk by
+// chunk, rotating kStages buffers, so that packing chunk k+1 overlaps the DMA of chunk k
+// and the decode of chunk k-1. A chunk's staging is [cluster of each request (u32) |
+// staged byte offset of each request (u32) | the packed rows, byte-packed].
+ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, uint8_t *d_out, hipStream_t s) {
+    const uint64_t L = h->d.row_bytes, G = h->d.group_rows;
+    const uint64_t magic = dev::div_magic((uint32_t)G);
+    h->req_g.resize(n);
+    h->req_rb.resize(n);
+    uint32_t *rg = h->req_g.data(), *rrb = h->req_rb.data();
+    const uint32_t *grb = h->h_rb.data();
+    h->pool->run(n, 8192, [&](uint64_t lo, uint64_t hi) {
+        for (uint64_t i = lo; i < hi; ++i) {
+            const uint64_t id = (uint64_t)ids[i];
+            const uint64_t g = G == 1 ? id : (uint64_t)(((unsigned __int128)id * magic) >> 64);
+            rg[i] = (uint32_t)g;
+            rrb[i] = grb[g];
+        }
+    });
+    // fixed rows per chunk so that any chunk fits: 8 B of tables + the largest packed row
+    const uint64_t per_chunk = std::max<uint64_t>(1, (kStageBytes - 64) / (8 + (uint64_t)h->max_rb));
+    constexpr uint64_t kBlk = 2048;
+    for (uint64_t i0 = 0; i0 < n; i0 += per_chunk) {
+        const uint64_t nc = std::min(per_chunk, n - i0);
+        const int b = h->next_stage;
+        h->next_stage = (h->next_stage + 1) % kStages;
+        ibp_status st = claim_stage(h, b, true);
+        if (st != IBP_OK) return st;
+        auto t0 = std::chrono::steady_clock::now();
+        uint8_t *stg = h->h_stage[b];
+        uint32_t *sg = reinterpret_cast<uint32_t *>(stg);
+        uint32_t *soff = sg + nc;
+        uint8_t *pay = stg + 8 * nc;
+        // staged offsets: block sums in parallel, a short scan over blocks, then every
+        // block writes its tables and copies its rows (prefetching a few rows ahead,
+        // since each row is a random read of ~rb bytes from host memory)
+        const uint64_t nblk = (nc + kBlk - 1) / kBlk;
+        h->blk_off.assign(nblk + 1, 0);
+        uint64_t *bo = h->blk_off.data();
+        h->pool->run(nblk, 1, [&](uint64_t lo, uint64_t hi) {
+            for (uint64_t k = lo; k < hi; ++k) {
+                uint64_t sum = 0;
+                const uint64_t a = i0 + k * kBlk, e = std::min(i0 + nc, a + kBlk);
+                for (uint64_t i = a; i < e; ++i) sum += rrb[i];
+                bo[k + 1] = sum;
+            }
+        });
+        for (uint64_t k = 0; k < nblk; ++k) bo[k + 1] += bo[k];
+        const uint64_t total_pay = bo[nblk];
+        const uint8_t *src_base = h->h_payload;
+        const uint64_t *goff = h->h_off.data();
+        h->pool->run(nblk, 1, [&](uint64_t lo, uint64_t hi) {
+            constexpr uint64_t kAhead = 8;
+            for (uint64_t k = lo; k < hi; ++k) {
+                const uint64_t a = i0 + k * kBlk, e = std::min(i0 + nc, a + kBlk);
+                uint64_t o = bo[k];
+                auto src_of = [&](uint64_t i) {
+                    const uint64_t g = rg[i], r = (uint64_t)ids[i] - g * G;
+                    return src_base + goff[g] + r * rrb[i];
+                };
+                for (uint64_t i = a; i < std::min(e, a + kAhead); ++i) {
+                    const uint8_t *p = src_of(i);
+                    for (uint32_t c = 0; c < rrb[i]; c += 64) __builtin_prefetch(p + c);
+                }
+                for (uint64_t i = a; i < e; ++i) {
+                    if (i + kAhead < e) {
+                        const uint8_t *p = src_of(i + kAhead);
+                        for (uint32_t c = 0; c < rrb[i + kAhead]; c += 64) __builtin_prefetch(p + c);
+                    }
+                    sg[i - i0] = rg[i];
+                    soff[i - i0] = (uint32_t)o;
+                    std::memcpy(pay + o, src_of(i), rrb[i]);
+                    o += rrb[i];
+                }
+            }
+        });
+        h->stats.host_pack_ns +=
+            (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0).count();
+        const uint64_t total = 8 * nc + total_pay;
+        IBP_HIP(h, hipMemcpyAsync(h->d_stage[b], stg, total, hipMemcpyHostToDevice, h->copy_stream));
+        IBP_HIP(h, hipEventRecord(h->ev_copied[b], h->copy_stream));
+        IBP_HIP(h, hipStreamWaitEvent(s, h->ev_copied[b], 0));
+        const uint8_t *dst = h->d_stage[b];
+        IBP_HIP(h, dev::launch_gather(h->ds, dst + 8 * nc, nullptr, reinterpret_cast<const uint32_t *>(dst),
+                                      reinterpret_cast<const uint32_t *>(dst) + nc, nc, d_out + i0 * L, h->d_err, s));
+        IBP_HIP(h, hipEventRecord(h->ev_free[b], s));
+        h->stage_used[b] = true;
+        h->stats.h2d_bytes += total;
+        h->stats.h2d_payload_bytes += total_pay;
+    }
+    return IBP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -288,7 +392,8 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     clear_error();
     if (!out) return fail(IBP_EINVAL, "handle output is null");
     *out = nullptr;
-    if (flags != IBP_OPEN_PAYLOAD_DEVICE && flags != IBP_OPEN_PAYLOAD_HOST)
+    if (flags != IBP_OPEN_PAYLOAD_DEVICE && flags != IBP_OPEN_PAYLOAD_HOST &&
+        flags != IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)
         return fail(IBP_EINVAL, "unknown open flags");
     StreamView v;
     ibp_status st = parse_stream(stream, stream_bytes, v);
@@ -336,9 +441,16 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
             (d.payload_bytes &&
              hipMemcpy(h->d_payload, v.payload(), d.payload_bytes, hipMemcpyHostToDevice) != hipSuccess))
             return bail(fail(IBP_EHIP, "payload upload failed"));
+        h->k_payload = h->d_payload;
     } else {
         st = setup_host_path(h, v);
         if (st != IBP_OK) return bail(st);
+        if (flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) {
+            void *dp = nullptr;
+            if (hipHostGetDevicePointer(&dp, h->h_payload, 0) != hipSuccess || !dp)
+                return bail(fail(IBP_EHIP, "pinned payload is not mapped for the device"));
+            h->k_payload = static_cast<const uint8_t *>(dp);
+        }
     }
     if (hipEventCreateWithFlags(&h->ev_ids, hipEventDisableTiming) != hipSuccess)
         return bail(fail(IBP_EHIP, "event creation failed"));
@@ -369,8 +481,8 @@ ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, vo
     if (out_cap / d.row_bytes < n_rows) return fail(IBP_ENOMEM, "output capacity too small");
     hipStream_t s = static_cast<hipStream_t>(stream);
     const uint64_t L = d.row_bytes, G = d.group_rows;
-    if (h->flags == IBP_OPEN_PAYLOAD_DEVICE) {
-        IBP_HIP(h, dev::launch_decompress(h->ds, h->d_payload, 0, d_out, first_row, n_rows, s));
+    if (h->flags != IBP_OPEN_PAYLOAD_HOST) {
+        IBP_HIP(h, dev::launch_decompress(h->ds, h->k_payload, 0, d_out, first_row, n_rows, s));
     } else {
         // chunks of whole groups whose packed bytes fit one staging buffer
         const uint64_t last = first_row + n_rows;
@@ -382,7 +494,7 @@ ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, vo
             const uint64_t bytes = h->h_off[gb] - h->h_off[ga];
             if (bytes > kStageBytes) return fail(IBP_EINVAL, "a group is larger than the staging buffer");
             const int b = h->next_stage;
-            h->next_stage ^= 1;
+            h->next_stage = (h->next_stage + 1) % kStages;
             st = claim_stage(h, b, false);
             if (st != IBP_OK) return st;
             if (bytes)
@@ -421,74 +533,20 @@ ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t
             return fail(IBP_ERANGE, "row id " + std::to_string(row_ids[i]) + " at position " + std::to_string(i) +
                                         " is outside [0, " + std::to_string(d.n_rows) + ")");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const uint64_t L = d.row_bytes, G = d.group_rows;
-    if (h->flags == IBP_OPEN_PAYLOAD_DEVICE) {
+    const uint64_t L = d.row_bytes;
+    if (h->flags != IBP_OPEN_PAYLOAD_HOST) {
         st = ensure_ids(h, n_ids);
         if (st != IBP_OK) return st;
         if (h->ids_pending) IBP_HIP(h, hipEventSynchronize(h->ev_ids));
         std::memcpy(h->h_ids, row_ids, n_ids * 8);
         IBP_HIP(h, hipMemcpyAsync(h->d_ids, h->h_ids, n_ids * 8, hipMemcpyHostToDevice, s));
-        IBP_HIP(h, dev::launch_gather(h->ds, h->d_payload, h->d_ids, nullptr, n_ids, d_out, h->d_err, s));
+        IBP_HIP(h, dev::launch_gather(h->ds, h->k_payload, h->d_ids, nullptr, nullptr, n_ids, d_out, h->d_err, s));
         IBP_HIP(h, hipEventRecord(h->ev_ids, s));
         h->ids_pending = true;
         h->stats.h2d_bytes += n_ids * 8;
     } else {
-        // Host packing: each chunk's staging holds [ids | staged offsets | packed rows].
-        uint64_t i0 = 0;
-        while (i0 < n_ids) {
-            // rows that fit: 12 bytes of tables + the packed row rounded to 4 bytes
-            uint64_t i1 = i0, used = 0;
-            while (i1 < n_ids) {
-                const uint64_t g = (uint64_t)row_ids[i1] / G;
-                const uint64_t need = 12 + round_up(h->h_rb[g], 4);
-                if (used + need + 8 > kStageBytes) break;
-                used += need;
-                ++i1;
-            }
-            if (i1 == i0) return fail(IBP_EINVAL, "a row is larger than the staging buffer");
-            const uint64_t nc = i1 - i0;
-            const int b = h->next_stage;
-            h->next_stage ^= 1;
-            st = claim_stage(h, b, true);
-            if (st != IBP_OK) return st;
-            auto t0 = std::chrono::steady_clock::now();
-            uint8_t *stg = h->h_stage[b];
-            int64_t *ids = reinterpret_cast<int64_t *>(stg);
-            uint32_t *soff = reinterpret_cast<uint32_t *>(stg + 8 * nc);
-            const uint64_t pay0 = round_up(8 * nc + 4 * nc, 16);
-            uint8_t *pay = stg + pay0;
-            // staged offsets (serial prefix sum), then parallel copies
-            uint64_t o = 0;
-            for (uint64_t k = 0; k < nc; ++k) {
-                const int64_t id = row_ids[i0 + k];
-                ids[k] = id;
-                soff[k] = (uint32_t)o;
-                o += round_up(h->h_rb[(uint64_t)id / G], 4);
-            }
-            const uint64_t total = pay0 + o;
-            h->pool->run(nc, 2048, [&](uint64_t lo, uint64_t hi) {
-                for (uint64_t k = lo; k < hi; ++k) {
-                    const uint64_t id = (uint64_t)ids[k], g = id / G, r = id - g * G;
-                    const uint32_t rb = h->h_rb[g];
-                    std::memcpy(pay + soff[k], h->h_payload + h->h_off[g] + r * rb, rb);
-                }
-            });
-            h->stats.host_pack_ns +=
-                (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0)
-                    .count();
-            IBP_HIP(h, hipMemcpyAsync(h->d_stage[b], stg, total, hipMemcpyHostToDevice, h->copy_stream));
-            IBP_HIP(h, hipEventRecord(h->ev_copied[b], h->copy_stream));
-            IBP_HIP(h, hipStreamWaitEvent(s, h->ev_copied[b], 0));
-            const uint8_t *dst = h->d_stage[b];
-            IBP_HIP(h, dev::launch_gather(h->ds, dst + pay0, reinterpret_cast<const int64_t *>(dst),
-                                          reinterpret_cast<const uint32_t *>(dst + 8 * nc), nc,
-                                          static_cast<uint8_t *>(d_out) + i0 * L, h->d_err, s));
-            IBP_HIP(h, hipEventRecord(h->ev_free[b], s));
-            h->stage_used[b] = true;
-            h->stats.h2d_bytes += total;
-            h->stats.h2d_payload_bytes += o;
-            i0 = i1;
-        }
+        st = gather_host_payload(h, row_ids, n_ids, static_cast<uint8_t *>(d_out), s);
+        if (st != IBP_OK) return st;
     }
     h->stats.calls += 1;
     h->stats.rows_out += n_ids;
@@ -502,12 +560,13 @@ ibp_status ibp_gather_decompress_device(ibp_handle *h, const int64_t *d_row_ids,
     CallScope cs(h);
     ibp_status st = check_handle(h, cs);
     if (st != IBP_OK) return st;
-    if (h->flags != IBP_OPEN_PAYLOAD_DEVICE)
-        return fail(IBP_EINVAL, "device row ids need a handle opened with IBP_OPEN_PAYLOAD_DEVICE");
+    if (h->flags == IBP_OPEN_PAYLOAD_HOST)
+        return fail(IBP_EINVAL, "device row ids need a handle whose kernels read the payload in place "
+                                "(IBP_OPEN_PAYLOAD_DEVICE or IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)");
     if (n_ids == 0) return IBP_OK;
     if (!d_row_ids || !d_out) return fail(IBP_EINVAL, "row ids or output is null");
     if (out_cap / h->d.row_bytes < n_ids) return fail(IBP_ENOMEM, "output capacity too small");
-    IBP_HIP(h, dev::launch_gather(h->ds, h->d_payload, d_row_ids, nullptr, n_ids, d_out, h->d_err,
+    IBP_HIP(h, dev::launch_gather(h->ds, h->k_payload, d_row_ids, nullptr, nullptr, n_ids, d_out, h->d_err,
                                   static_cast<hipStream_t>(stream)));
     h->stats.calls += 1;
     h->stats.rows_out += n_ids;

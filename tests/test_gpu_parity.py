@@ -16,7 +16,8 @@ from workloads import CONFIGS, gen_all_rows, gen_rows, gnn_batch_ids, structured
 
 pytestmark = pytest.mark.gpu
 
-FLAGS = {"device": ibp.IBP_OPEN_PAYLOAD_DEVICE, "host": ibp.IBP_OPEN_PAYLOAD_HOST}
+FLAGS = {"device": ibp.IBP_OPEN_PAYLOAD_DEVICE, "host": ibp.IBP_OPEN_PAYLOAD_HOST,
+         "zero_copy": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY}
 
 
 def say(*a):
@@ -72,7 +73,7 @@ SMALL = [("floats", 300, 400, 32), ("random", 97, 12, 5), ("specials", 70, 16, 7
          ("alternating", 45, 520, 9)]
 
 
-@pytest.mark.parametrize("flags", ["device", "host"])
+@pytest.mark.parametrize("flags", ["device", "host", "zero_copy"])
 @pytest.mark.parametrize("kind,n,L,G", SMALL, ids=[f"{c[0]}-{c[1]}x{c[2]}-G{c[3]}" for c in SMALL])
 def test_decompress_small(torch, kind, n, L, G, flags):
     rows = structured_rows(kind, n, L, seed=n + 3 * L)
@@ -88,7 +89,8 @@ def test_decompress_small(torch, kind, n, L, G, flags):
     assert np.array_equal(got, want[a:b])
 
 
-@pytest.mark.parametrize("mode", ["device_payload_host_ids", "device_payload_device_ids", "host_payload"])
+@pytest.mark.parametrize("mode", ["device_payload_host_ids", "device_payload_device_ids", "host_payload",
+                                  "zero_copy_host_ids", "zero_copy_device_ids"])
 @pytest.mark.parametrize("kind,n,L,G", SMALL, ids=[f"{c[0]}-{c[1]}x{c[2]}-G{c[3]}" for c in SMALL])
 def test_gather_small(torch, kind, n, L, G, mode):
     rows = structured_rows(kind, n, L, seed=n + 3 * L)
@@ -98,8 +100,9 @@ def test_gather_small(torch, kind, n, L, G, mode):
                           [0, n - 1, n - 1]]).astype(np.int64)
     want = oracle.decode_rows(stream, ids, L)
     say(f"[gather] {kind} n={n} L={L} G={G} mode={mode} n_ids={ids.size}")
-    flags = ibp.IBP_OPEN_PAYLOAD_HOST if mode == "host_payload" else ibp.IBP_OPEN_PAYLOAD_DEVICE
-    got, errs = gpu_gather(torch, stream, ids, L, flags, device_ids=mode == "device_payload_device_ids")
+    flags = (ibp.IBP_OPEN_PAYLOAD_HOST if mode == "host_payload" else
+             ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero_copy") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
+    got, errs = gpu_gather(torch, stream, ids, L, flags, device_ids=mode.endswith("device_ids"))
     assert errs == 0
     assert np.array_equal(got, want)
 
@@ -154,6 +157,11 @@ def test_edge_cases(torch):
         with pytest.raises(ibp.IbpError) as e:
             ibp.ibp_gather_decompress_device(h, d_ids, out3, out_cap=5 * 64)
         assert e.value.status == ibp.IBP_EINVAL
+    with ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) as h:
+        out4 = _out(torch, 5, 64)
+        ibp.ibp_gather_decompress_device(h, d_ids, out4, out_cap=5 * 64)
+        assert ibp.ibp_device_errors(h) == 3
+        assert np.array_equal(_rows(out4, 5, 64), got)
 
 
 def test_open_rejects_corrupt_stream(torch):
@@ -224,10 +232,11 @@ def test_gnn_gather_full(torch):
     ids = gnn_batch_ids(cfg.n_rows, cfg.extra["seeds"], cfg.extra["fanouts"], batch_index=0)
     sample = np.random.default_rng(5).choice(ids.size, 3000, replace=False)
     want_sample = oracle.decode_rows(stream, ids[sample], cfg.row_bytes)
-    for mode in ("device_ids", "host_ids", "host_payload"):
+    for mode in ("device_ids", "host_ids", "host_payload", "zero_copy_device_ids"):
         say(f"[gnn gather] mode={mode} n_ids={ids.size}")
-        flags = ibp.IBP_OPEN_PAYLOAD_HOST if mode == "host_payload" else ibp.IBP_OPEN_PAYLOAD_DEVICE
-        got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=mode == "device_ids")
+        flags = (ibp.IBP_OPEN_PAYLOAD_HOST if mode == "host_payload" else
+                 ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero_copy") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
+        got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=mode.endswith("device_ids"))
         assert errs == 0
         assert np.array_equal(got, rows[ids])
         assert np.array_equal(got[sample], want_sample)
