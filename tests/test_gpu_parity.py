@@ -240,3 +240,86 @@ def test_gnn_gather_full(torch):
         assert errs == 0
         assert np.array_equal(got, rows[ids])
         assert np.array_equal(got[sample], want_sample)
+
+
+# ---------------------------------------------------------------- full-size workloads
+# These hold tens of GB of host memory (the raw tables) and take a minute or two each,
+# mostly drawing the synthetic rows.
+
+def _full_stream(cfg):
+    import time
+    t = time.time()
+    rows = gen_all_rows(cfg)
+    say(f"[{cfg.key}] drew {rows.shape[0]} x {rows.shape[1]} B in {time.time() - t:.0f}s")
+    t = time.time()
+    stream = ibp.ibp_compress(rows, cfg.group_rows)
+    d = ibp.ibp_describe(stream)
+    say(f"[{cfg.key}] compressed in {time.time() - t:.0f}s: payload {d['payload_bytes'] / 1e9:.2f} GB "
+        f"(CR {rows.nbytes / d['payload_bytes']:.2f}), stream {d['stream_bytes'] / 1e9:.2f} GB")
+    return rows, stream, d
+
+
+@pytest.mark.timeout(900)
+def test_dlrm_full(torch):
+    """26 tables x 4M rows x 128 fp32 (53 GB raw), one batch of 2,048 x 26 Zipf lookups."""
+    import gc
+    from workloads import dlrm_batch_ids
+    cfg = CONFIGS["dlrm"]
+    rows, stream, d = _full_stream(cfg)
+    _sampled_groups_match_oracle(stream, rows, cfg.group_rows, cfg.row_bytes, d["n_groups"], 48, 7)
+    x = cfg.extra
+    ids = dlrm_batch_ids(x["tables"], x["rows_per_table"], x["batch"], x["zipf_s"], batch_index=0)
+    want = rows[ids]
+    sample = np.random.default_rng(9).choice(ids.size, 2000, replace=False)
+    assert np.array_equal(oracle.decode_rows(stream, ids[sample], cfg.row_bytes), want[sample])
+    for mode in ("device_ids", "zero_copy_device_ids"):
+        say(f"[dlrm] gather mode={mode} n_ids={ids.size}")
+        flags = ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE
+        got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=True)
+        assert errs == 0
+        assert np.array_equal(got, want)       # [2048, 26, 128] fp32, sample-major
+    del rows, stream
+    gc.collect()
+
+
+@pytest.mark.timeout(900)
+def test_big_gnn_full(torch):
+    """111M rows x 128 fp32 (57 GB raw), G = 64, a 3-hop (15,10,5) minibatch of ~3.69M rows."""
+    import gc
+    cfg = CONFIGS["big_gnn"]
+    rows, stream, d = _full_stream(cfg)
+    _sampled_groups_match_oracle(stream, rows, cfg.group_rows, cfg.row_bytes, d["n_groups"], 48, 8)
+    ids = gnn_batch_ids(cfg.n_rows, cfg.extra["seeds"], cfg.extra["fanouts"], batch_index=0)
+    want = rows[ids]
+    sample = np.random.default_rng(10).choice(ids.size, 2000, replace=False)
+    assert np.array_equal(oracle.decode_rows(stream, ids[sample], cfg.row_bytes), want[sample])
+    for mode in ("device_ids", "zero_copy_device_ids"):
+        say(f"[big_gnn] gather mode={mode} n_ids={ids.size}")
+        flags = ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE
+        got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=True)
+        assert errs == 0
+        assert np.array_equal(got, want)
+    del rows, stream, want
+    gc.collect()
+
+
+@pytest.mark.timeout(900)
+def test_kv_full(torch):
+    """All 32 layers of the bf16 KV workload (4 GiB raw), streamed layer by layer."""
+    import gc
+    cfg = CONFIGS["kv_bf16"]
+    rows, stream, d = _full_stream(cfg)
+    _sampled_groups_match_oracle(stream, rows, cfg.group_rows, cfg.row_bytes, d["n_groups"], 48, 11)
+    n = cfg.extra["rows_per_layer"]
+    for flags in (ibp.IBP_OPEN_PAYLOAD_DEVICE, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY, ibp.IBP_OPEN_PAYLOAD_HOST):
+        say(f"[kv full] flags={flags}")
+        with ibp.ibp_open(stream, 0, flags) as h:
+            out = torch.empty(n * cfg.row_bytes, dtype=torch.uint8, device="cuda")
+            for layer in range(cfg.extra["layers"]):
+                ibp.ibp_decompress(h, layer * n, n, out)
+                got = out.cpu().numpy().reshape(n, cfg.row_bytes)
+                assert np.array_equal(got, rows[layer * n:(layer + 1) * n]), layer
+    sample = np.random.default_rng(12).integers(0, cfg.n_rows, 2000)
+    assert np.array_equal(oracle.decode_rows(stream, sample, cfg.row_bytes), rows[sample])
+    del rows, stream
+    gc.collect()
