@@ -1,22 +1,27 @@
 #!/usr/bin/env python3
 """Benchmark of the IBP decompression hot path on one MI355X.
 
-Workload (default): the GNN minibatch gather -- 2,400,000 rows x 100 fp32 features
-(values N(0,1) rounded to 8 mantissa bits), clusters of 32 rows, minibatches of 1,024
-seed rows with a 2-hop (15, 10) uniform fanout (about 164k unique sorted row ids). The
-compressed stream and every batch's ids are resident in HBM before timing starts; one
-step = one ibp_gather_decompress_device call over one minibatch (a different batch per
-step). `value` is decompressed output bytes per second of the timed steps.
+Default workload (`--workload gnn_gather`): the GNN minibatch gather -- 2,400,000 rows x
+100 fp32 features (N(0,1) rounded to 8 mantissa bits), clusters of 32 rows, minibatches of
+1,024 seed rows with a 2-hop (15, 10) uniform fanout (about 164k unique sorted row ids).
+The compressed stream and every batch's ids are resident in HBM before timing starts; one
+step = one ibp_gather_decompress_device call over one minibatch (a different batch each
+step). `value` is decompressed output bytes per second over the timed steps.
+
+Other workloads (`--workload`): `dlrm` (26 tables x 4M x 128 fp32, batches of 2,048 x 26
+Zipf lookups), `big_gnn` (111M x 128 fp32, 3-hop minibatches), both gathers like the
+default; `kv_bf16` (one step = one 128 MiB layer of the bf16 KV cache through
+ibp_decompress) and `tiny_gnn` (one step = the whole 4,096 x 128 fp32 tensor).
 
 Also reported on the same JSON line:
-  roofline      the gather kernel's algorithmic HBM bytes per launch (ids + packed rows
-                read + rows written + Mask/Bitval/index once per distinct cluster) over
-                its average duration from HIP events, against 8 TB/s;
+  roofline      the step kernel's algorithmic HBM bytes per launch over its average
+                duration from HIP events, against 8 TB/s; `traffic` comes from the
+                committed rocprofv3 counter summary of that kernel on that workload while
+                the kernel source is unchanged (else null); plus a plain 1 GiB device copy;
   cpu_baseline  the CPU oracle (single thread, bit-serial) decoding a bounded sample of
-                one minibatch, in the same unit;
-  e2e           the PCIe-inclusive paths (payload in pinned host memory): the same gather
-                with host packing + staged DMA and with GPU-initiated zero-copy reads, and
-                8 layers of the bf16 KV workload streamed both ways; effective output GB/s
+                one step's rows, in the same unit;
+  e2e           the PCIe-inclusive paths (payload in pinned host memory): host-packed
+                staging + DMA and GPU-initiated zero-copy reads; effective output GB/s
                 next to raw pinned H2D GB/s and the compression ratio of the bytes needed.
 """
 import argparse
@@ -35,27 +40,45 @@ sys.path.insert(0, ROOT)
 METRIC = "decompressed GB/s (HBM roofline %) + effective H2D GB/s vs raw PCIe"
 HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2605_30728_amd", "csrc", "ibp_kernels.hip")
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "k_gather_rows_gnn_gather.md")
+GATHERS = ("gnn_gather", "dlrm", "big_gnn")
+STREAMS = ("kv_bf16", "tiny_gnn")
+DESCRIPTIONS = {
+    "gnn_gather": "gnn_gather: 2.4M x 100 fp32 rows (N(0,1), 8 mantissa bits), G=32, 1,024 seeds, "
+                  "fanout (15,10), device-resident stream and ids",
+    "dlrm": "dlrm: 26 tables x 4M x 128 fp32 (U(-0.05,0.05) in 1/4096 steps), G=32, batch 2,048 x 26 "
+            "Zipf(1.05) lookups, device-resident stream and ids",
+    "big_gnn": "big_gnn: 111M x 128 fp32 (70% zeros, else U(0,1) in 1/1024 steps), G=64, 4,096 seeds, "
+               "fanout (15,10,5), device-resident stream and ids",
+    "kv_bf16": "kv_bf16: 32 layers x [K,V] x 8 heads x 32,768 tokens x 128 bf16, G=32 tokens, one layer "
+               "(524,288 rows) per step, device-resident stream",
+    "tiny_gnn": "tiny_gnn: 4,096 x 128 fp32 (k/256, 50% zeros), G=32, all rows per step, device-resident stream",
+}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(ids, G, L, rb_of_group):
-    """HBM bytes one gather launch must move: ids, packed rows, output rows, and the
-    Mask/Bitval + index entry of every distinct cluster touched."""
-    g = ids // G
-    distinct = np.unique(g).size
-    return int(ids.size * 8 + rb_of_group[g].sum() + ids.size * L + distinct * (2 * L + 8))
+def wk_for(W):
+    return 1 if W <= 64 else 2 if W <= 128 else 4 if W <= 256 else 8
 
 
-def measured_traffic():
-    """HBM bytes per gather launch from the committed rocprofv3 counter summary, or None
-    when the kernel source has changed since the counters were taken."""
-    if not os.path.exists(TRAFFIC_PROFILE):
+def kernel_name(workload, W):
+    k = wk_for(W)
+    if workload in GATHERS:
+        rb = {1: 8, 2: 4, 4: 2, 8: 1}[k]
+        return f"k_gather_rows<{k},{rb}>" if W <= 512 else "k_gather_tiled"
+    return f"k_decompress<{k},{ {1: 4, 2: 4, 4: 2, 8: 1}[k] }>"
+
+
+def measured_traffic(workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this workload,
+    or None when the kernel source has changed since the counters were taken."""
+    kind = "k_gather_rows" if workload in GATHERS else "k_decompress"
+    path = os.path.join(ROOT, "profiles", f"{kind}_{workload}.md")
+    if not os.path.exists(path):
         return None
-    text = open(TRAFFIC_PROFILE).read()
+    text = open(path).read()
     m_hash = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
     m_bytes = re.search(r"traffic_bytes_per_launch:\s*(\d+)", text)
     if not m_hash or not m_bytes:
@@ -97,64 +120,93 @@ def raw_h2d_gbs(torch, nbytes, reps=5):
     return nbytes * reps / (s.elapsed_time(e) * 1e-3) / 1e9
 
 
-def pcie_legs(torch, ibp, stream, rows, timed, warm, L, G, rb_of_group):
-    """The PCIe-inclusive legs (never `value`): the same minibatch gather with the payload
-    in pinned host memory, (a) host-packed rows through rotating staging + DMA and
-    (b) GPU-initiated zero-copy reads by the gather kernel; and (c) streaming the layers
-    of the bf16 KV workload through ibp_decompress both ways. Effective GB/s = output bytes
-    / wall time; compared with raw pinned H2D and the ratio of output bytes to the packed
-    bytes the path needs (packed rows + 8 B of per-row tables for gathers)."""
-    from workloads import CONFIGS, gen_rows
+class Steps:
+    """The per-step units of a workload: row-id batches (gathers) or row ranges (streams),
+    with the algorithmic HBM bytes one launch over each must move."""
+
+    def __init__(self, workload, cfg, n_steps, index, rb_of_group):
+        from workloads import dlrm_batch_ids, gnn_batch_ids
+        self.workload, self.cfg = workload, cfg
+        G, L = cfg.group_rows, cfg.row_bytes
+        if workload in GATHERS:
+            distinct = min(n_steps, {"gnn_gather": 64, "dlrm": 8, "big_gnn": 8}[workload])
+            x = cfg.extra
+            if workload == "dlrm":
+                self.units = [dlrm_batch_ids(x["tables"], x["rows_per_table"], x["batch"], x["zipf_s"], batch_index=b)
+                              for b in range(distinct)]
+            else:
+                self.units = [gnn_batch_ids(cfg.n_rows, x["seeds"], x["fanouts"], batch_index=b)
+                              for b in range(distinct)]
+            # ids, packed rows read, rows written, and Mask/Bitval + index entry per cluster
+            self.alg = [int(u.size * 8 + rb_of_group[u // G].sum() + u.size * L + np.unique(u // G).size * (2 * L + 8))
+                        for u in self.units]
+            self.rows = [u.size for u in self.units]
+        else:
+            per = cfg.extra["rows_per_layer"] if workload == "kv_bf16" else cfg.n_rows
+            self.units = [(f, per) for f in range(0, cfg.n_rows, per)]
+            self.alg = []
+            for f, n in self.units:
+                g0, g1 = f // G, (f + n - 1) // G + 1
+                self.alg.append(int(index[g1] - index[g0] + n * L + (g1 - g0) * (2 * L + 8)))
+            self.rows = [n for _, n in self.units]
+
+    def __len__(self):
+        return len(self.units)
+
+    def row_ids(self, k):
+        u = self.units[k % len(self)]
+        return u if self.workload in GATHERS else np.arange(u[0], u[0] + u[1], dtype=np.int64)
+
+
+def pcie_legs(torch, ibp, args, stream, rows, steps, L, G, rb_of_group, index):
+    """The PCIe-inclusive legs (never `value`): the same steps with the payload in pinned
+    host memory, (a) through host-packed staging + DMA on a side stream (host packing of
+    the requested rows for gathers, whole cluster ranges for streams) and (b) read by the
+    decode kernels themselves (GPU-initiated zero-copy). Effective GB/s = output bytes /
+    wall time; cr = output bytes / packed bytes the path needs (packed rows, plus 8 B of
+    per-row tables for gathers)."""
     raw = raw_h2d_gbs(torch, 1 << 30)
-    out = torch.empty(max(b.size for b in timed + warm) * L, dtype=torch.uint8, device="cuda")
-    packed = sum(int(rb_of_group[b // G].sum()) + 8 * b.size for b in timed)
-    out_total = sum(b.size * L for b in timed)
-    cr = out_total / packed
-    res = {"raw_h2d_GBps_1GiB": round(raw, 2), "steps": len(timed)}
-    for mode, flags in (("gather_host_pack", ibp.IBP_OPEN_PAYLOAD_HOST),
-                        ("gather_zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)):
+    n_e2e = min(args.e2e_steps, max(len(steps), 1) * 4)
+    sel = [k % len(steps) for k in range(n_e2e)]
+    out = torch.empty(max(steps.rows) * L, dtype=torch.uint8, device="cuda")
+    out_total = sum(steps.rows[k] * L for k in sel)
+    if steps.workload in GATHERS:
+        need = sum(int(rb_of_group[steps.units[k] // G].sum()) + 8 * steps.rows[k] for k in sel)
+    else:
+        need = 0
+        for k in sel:
+            f, n = steps.units[k]
+            need += int(index[(f + n - 1) // G + 1] - index[f // G])
+    cr = out_total / need
+    res = {"raw_h2d_GBps_1GiB": round(raw, 2), "steps": n_e2e, "cr": round(cr, 3)}
+
+    def run(h, k):
+        if steps.workload in GATHERS:
+            ibp.ibp_gather_decompress(h, steps.units[k], out)
+        else:
+            f, n = steps.units[k]
+            ibp.ibp_decompress(h, f, n, out)
+
+    for mode, flags in (("staged_dma", ibp.IBP_OPEN_PAYLOAD_HOST), ("zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)):
         h = ibp.ibp_open(stream, 0, flags)
-        for b in warm:
-            ibp.ibp_gather_decompress(h, b, out)
+        run(h, sel[0])
         torch.cuda.synchronize()
         ibp.ibp_reset_stats(h)
         t = time.perf_counter()
-        for b in timed:
-            ibp.ibp_gather_decompress(h, b, out)
+        for k in sel:
+            run(h, k)
         torch.cuda.synchronize()
         dt = time.perf_counter() - t
         st = ibp.ibp_get_stats(h)
-        got = out[:timed[-1].size * L].cpu().numpy().reshape(-1, L)
-        assert np.array_equal(got, rows[timed[-1]]), mode
+        last = sel[-1]
+        got = out[:steps.rows[last] * L].cpu().numpy().reshape(-1, L)
+        assert np.array_equal(got, rows[steps.row_ids(last)]), mode
         ibp.ibp_close(h)
         eff = out_total / dt / 1e9
-        res[mode] = {"effective_GBps": round(eff, 2), "cr": round(cr, 3),
-                     "effective_over_cr_raw": round(eff / (cr * raw), 3),
-                     "host_pack_ms_per_batch": round(st["host_pack_ns"] / len(timed) / 1e6, 3)}
-        log(f"[bench] e2e {mode}: {eff:.1f} GB/s effective ({eff / (cr * raw):.2f} of CR x raw)")
-    kv = CONFIGS["kv_bf16"]
-    n = kv.extra["rows_per_layer"]
-    layers = 8
-    krows = gen_rows(kv, 0, layers * n)
-    ks = ibp.ibp_compress(krows, kv.group_rows)
-    kcr = layers * n * kv.row_bytes / ibp.ibp_describe(ks)["payload_bytes"]
-    kout = torch.empty(n * kv.row_bytes, dtype=torch.uint8, device="cuda")
-    for mode, flags in (("kv_stream_staged_dma", ibp.IBP_OPEN_PAYLOAD_HOST),
-                        ("kv_stream_zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)):
-        h = ibp.ibp_open(ks, 0, flags)
-        ibp.ibp_decompress(h, 0, n, kout)
-        torch.cuda.synchronize()
-        t = time.perf_counter()
-        for layer in range(layers):
-            ibp.ibp_decompress(h, layer * n, n, kout)
-        torch.cuda.synchronize()
-        dt = time.perf_counter() - t
-        assert np.array_equal(kout.cpu().numpy().reshape(-1, kv.row_bytes), krows[(layers - 1) * n:]), mode
-        ibp.ibp_close(h)
-        eff = layers * n * kv.row_bytes / dt / 1e9
-        res[mode] = {"effective_GBps": round(eff, 2), "cr": round(kcr, 3),
-                     "effective_over_cr_raw": round(eff / (kcr * raw), 3), "layers": layers}
-        log(f"[bench] e2e {mode}: {eff:.1f} GB/s effective ({eff / (kcr * raw):.2f} of CR x raw)")
+        res[mode] = {"effective_GBps": round(eff, 2), "effective_over_cr_raw": round(eff / (cr * raw), 3),
+                     "host_pack_ms_per_step": round(st["host_pack_ns"] / n_e2e / 1e6, 3)}
+        log(f"[bench] e2e {mode}: {eff:.1f} GB/s effective ({eff / (cr * raw):.2f} of CR x raw, "
+            f"raw {raw:.1f} GB/s, CR {cr:.2f})")
     return res
 
 
@@ -163,6 +215,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="gnn_gather", choices=list(GATHERS + STREAMS))
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-e2e", action="store_true")
@@ -175,14 +228,15 @@ def main():
 
     import torch
     import paper_2605_30728_amd as ibp
-    from workloads import CONFIGS, gen_all_rows, gnn_batch_ids
+    from workloads import CONFIGS, gen_all_rows
 
-    cfg = CONFIGS["gnn_gather"]
-    G, L = cfg.group_rows, cfg.row_bytes
+    wl = args.workload
+    cfg = CONFIGS[wl]
+    G, L, W = cfg.group_rows, cfg.row_bytes, cfg.row_bytes // 4
     K, Wm = args.steps, args.warmup
     t = time.time()
     rows = gen_all_rows(cfg)
-    log(f"[bench] generated {cfg.n_rows} x {L} B rows in {time.time() - t:.1f}s")
+    log(f"[bench] {wl}: generated {cfg.n_rows} x {L} B rows in {time.time() - t:.1f}s")
     t = time.time()
     threads = min(16, os.cpu_count() or 1)
     stream = ibp.ibp_compress(rows, G, n_threads=threads)
@@ -195,17 +249,21 @@ def main():
     log(f"[bench] compressed in {compress_s:.2f}s ({threads} threads): payload {d['payload_bytes'] / 1e6:.1f} MB, "
         f"stream {d['stream_bytes'] / 1e6:.1f} MB, raw {cfg.n_rows * L / 1e6:.1f} MB")
 
-    batches = [gnn_batch_ids(cfg.n_rows, cfg.extra["seeds"], cfg.extra["fanouts"], batch_index=b)
-               for b in range(Wm + K)]
-    d_batches = [torch.from_numpy(b).cuda() for b in batches]
-    max_n = max(b.size for b in batches)
-    out = torch.empty(max_n * L, dtype=torch.uint8, device="cuda")
-    alg = [algorithmic_bytes(b, G, L, rb_of_group) for b in batches]
-
+    steps = Steps(wl, cfg, Wm + K, index, rb_of_group)
+    out = torch.empty(max(steps.rows) * L, dtype=torch.uint8, device="cuda")
     h = ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_DEVICE)
-    log(f"[bench] opened on cuda:0; warmup {Wm} steps, timing {K} steps")
-    for b in range(Wm):
-        ibp.ibp_gather_decompress_device(h, d_batches[b], out)
+    if wl in GATHERS:
+        d_units = [torch.from_numpy(u).cuda() for u in steps.units]
+
+        def step(k):
+            ibp.ibp_gather_decompress_device(h, d_units[k % len(steps)], out)
+    else:
+        def step(k):
+            f, n = steps.units[k % len(steps)]
+            ibp.ibp_decompress(h, f, n, out)
+    log(f"[bench] opened on cuda:0; {len(steps)} distinct step inputs; warmup {Wm} steps, timing {K} steps")
+    for k in range(Wm):
+        step(k)
     torch.cuda.synchronize()
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
@@ -213,25 +271,24 @@ def main():
     t0 = time.perf_counter()
     for k in range(K):
         ev[k][0].record()
-        ibp.ibp_gather_decompress_device(h, d_batches[Wm + k], out)
+        step(Wm + k)
         ev[k][1].record()
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    wall = t1 - t0
-    out_bytes = sum(batches[Wm + k].size * L for k in range(K))
+    wall = time.perf_counter() - t0
+    out_bytes = sum(steps.rows[(Wm + k) % len(steps)] * L for k in range(K))
     kern_ms = float(np.mean([s.elapsed_time(e) for s, e in ev]))
-    alg_avg = float(np.mean(alg[Wm:]))
+    alg_avg = float(np.mean([steps.alg[(Wm + k) % len(steps)] for k in range(K)]))
     achieved = alg_avg / (kern_ms * 1e-3) / 1e9
     value = out_bytes / wall / 1e9
-    # correctness of the last timed batch against the original rows
-    last = batches[Wm + K - 1]
-    got = out[:last.size * L].cpu().numpy().reshape(last.size, L)
-    if not np.array_equal(got, rows[last]):
-        log("[bench] ERROR: gathered rows differ from the originals")
+    last = (Wm + K - 1) % len(steps)
+    got = out[:steps.rows[last] * L].cpu().numpy().reshape(-1, L)
+    if not np.array_equal(got, rows[steps.row_ids(last)]):
+        log("[bench] ERROR: decompressed rows differ from the originals")
         sys.exit(1)
     assert ibp.ibp_device_errors(h) == 0
+    ibp.ibp_close(h)
     copy_gbs = d2d_copy_gbs(torch)
-    traffic = measured_traffic()
+    traffic = measured_traffic(wl)
     log(f"[bench] {K} steps in {wall * 1e3:.2f} ms: {value:.1f} GB/s decompressed; kernel {kern_ms * 1e3:.1f} us "
         f"avg, {achieved:.0f} GB/s algorithmic ({achieved / HBM_PEAK_GBS:.1%} of HBM peak); "
         f"plain 1 GiB d2d copy {copy_gbs:.0f} GB/s")
@@ -239,8 +296,8 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        ids = batches[Wm]
-        probe = ids[:400]
+        ids = steps.row_ids(last)
+        probe = ids[:min(400, ids.size)]
         t = time.perf_counter()
         oracle.decode_rows(stream, probe, L)
         per_row = (time.perf_counter() - t) / probe.size
@@ -250,31 +307,26 @@ def main():
         cpu_s = time.perf_counter() - t
         assert np.array_equal(ref, rows[ids[:m]])
         cpu = {"value": round(m * L / cpu_s / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
-               "sample": f"bit-serial oracle decode of the first {m} of {ids.size} rows of one minibatch "
+               "sample": f"bit-serial oracle decode of the first {m} of {ids.size} rows of one step "
                          f"({cpu_s:.1f} s, 1 thread)"}
         log(f"[bench] cpu oracle: {cpu['value'] * 1e3:.2f} MB/s over {m} rows")
 
     e2e = None
     if not args.no_e2e:
-        e2e = pcie_legs(torch, ibp, stream, rows, batches[Wm:Wm + args.e2e_steps], batches[:3], L, G,
-                        rb_of_group)
-    ibp.ibp_close(h)
+        e2e = pcie_legs(torch, ibp, args, stream, rows, steps, L, G, rb_of_group, index)
 
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": Wm,
         "ms_per_step": round(wall * 1e3 / K, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "u32", "data": "synthetic",
-        "config": {"workload": "gnn_gather: 2.4M x 100 fp32 rows (N(0,1), 8 mantissa bits), G=32, "
-                               "1,024 seeds, fanout (15,10), device-resident stream and ids",
-                   "rows": cfg.n_rows, "row_bytes": L, "group_rows": G,
-                   "batch_rows_avg": round(float(np.mean([b.size for b in batches[Wm:]])), 1),
+        "config": {"workload": DESCRIPTIONS[wl], "rows": cfg.n_rows, "row_bytes": L, "group_rows": G,
+                   "rows_per_step_avg": round(float(np.mean(steps.rows)), 1),
                    "payload_cr": round(cfg.n_rows * L / d["payload_bytes"], 3),
                    "stream_cr": round(cfg.n_rows * L / d["stream_bytes"], 3)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": "k_gather_rows<2,4>", "kernel_us": round(kern_ms * 1e3, 2),
-                     "algorithmic_bytes_per_launch": int(alg_avg),
-                     "d2d_copy_GBps": round(copy_gbs, 1)},
+                     "kernel": kernel_name(wl, W), "kernel_us": round(kern_ms * 1e3, 2),
+                     "algorithmic_bytes_per_launch": int(alg_avg), "d2d_copy_GBps": round(copy_gbs, 1)},
         "cpu_baseline": cpu,
         "e2e": e2e,
     }

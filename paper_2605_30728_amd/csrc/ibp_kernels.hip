@@ -525,32 +525,52 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
 #pragma unroll
         for (int u = 0; u < RB; ++u)
             load_row_meta<K>(meta[u], s.meta + rd64(g_lo, g_hi, slot_of(base_i + u)) * 2ull * W, W);
-        uint32_t nm[RB][K], bv[RB][K], d0[RB][K], d1[RB][K], bit[RB][K], nh[RB];
+        // per row: variant positions, Bitval, bit offsets of the words inside the packed
+        // row (without the row's byte misalignment bit0), hole iterations, packed bits
+        uint32_t nm[RB][K], bv[RB][K], ofs[RB][K], d0[RB][K], d1[RB][K], nh[RB], tot[RB], bit0[RB];
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
+            const int up = u > 0 ? u - 1 : 0;
             const uint32_t i = slot_of(base_i + u);
-            uint32_t cntw[K], runs = 0;
+            // sorted ids put rows of one cluster next to each other: a row whose cluster
+            // is its predecessor's reuses that row's offsets and hole count (uniform branch)
+            const bool same = u > 0 && rd64(g_lo, g_hi, i) == rd64(g_lo, g_hi, slot_of(base_i + up));
+            if (same) {
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
-                const bool in_row = l + kWave * j < W;
-                nm[u][j] = in_row ? ~meta[u].m[j] : 0u;
-                bv[u][j] = in_row ? meta[u].b[j] : 0u;
-                cntw[j] = (uint32_t)__builtin_popcount(nm[u][j]);
-                runs = max(runs, run_count(nm[u][j]));
+                for (int j = 0; j < K; ++j) {
+                    nm[u][j] = nm[up][j];
+                    bv[u][j] = bv[up][j];
+                    ofs[u][j] = ofs[up][j];
+                }
+                nh[u] = nh[up];
+                tot[u] = tot[up];
+            } else {
+                uint32_t cntw[K], runs = 0;
+#pragma unroll
+                for (int j = 0; j < K; ++j) {
+                    const bool in_row = l + kWave * j < W;
+                    nm[u][j] = in_row ? ~meta[u].m[j] : 0u;
+                    bv[u][j] = in_row ? meta[u].b[j] : 0u;
+                    cntw[j] = (uint32_t)__builtin_popcount(nm[u][j]);
+                    runs = max(runs, run_count(nm[u][j]));
+                }
+                tot[u] = row_offsets<K>(cntw, ofs[u]);
+                const uint32_t max_runs = wave_max(runs);
+                nh[u] = max_runs ? max_runs - 1u : 0u;
             }
-            const uint32_t c = row_offsets<K>(cntw, bit[u]);
-            const uint32_t max_runs = wave_max(runs);
-            nh[u] = max_runs ? max_runs - 1u : 0u;
-            const uint64_t rb = (c + 7u) >> 3;
+            const uint64_t rb = (tot[u] + 7u) >> 3;
             uint64_t rbyte;
             if constexpr (STAGED) rbyte = (uint32_t)__builtin_amdgcn_readlane((int)so, (int)i);
-            else rbyte = rd64(off_lo, off_hi, i) + (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)r_l, (int)i) * rb;
+            else {
+                const uint64_t off = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)off_hi, (int)i) << 32) |
+                                     (uint32_t)__builtin_amdgcn_readlane((int)off_lo, (int)i);
+                rbyte = off + (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)r_l, (int)i) * rb;
+            }
             const uint32_t *__restrict__ p = pay32 + (rbyte >> 2);
-            const uint32_t bit0 = ((uint32_t)rbyte & 3u) * 8u;
+            bit0[u] = ((uint32_t)rbyte & 3u) * 8u;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-                bit[u][j] += bit0;
-                const uint32_t q = bit[u][j] >> 5;
+                const uint32_t q = (ofs[u][j] + bit0[u]) >> 5;
                 d0[u][j] = p[q];
                 d1[u][j] = p[q + 1];
             }
@@ -559,7 +579,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
 #pragma unroll
         for (int u = 0; u < RB; ++u)
 #pragma unroll
-            for (int j = 0; j < K; ++j) x[u][j] = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], bit[u][j]);
+            for (int j = 0; j < K; ++j)
+                x[u][j] = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], ofs[u][j] + bit0[u]);
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
             const uint32_t i = base_i + u;
@@ -597,14 +618,20 @@ hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_
                              uint64_t first, uint64_t n, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     const uint64_t g0 = first / s.G, g1 = (first + n - 1) / s.G;
-    const uint32_t rpu = s.G <= 64 ? s.G : 64;
+    // rows per wave: a whole cluster (at most 64 rows), halved while the launch would have
+    // fewer than ~16k waves (2 per wave slot of the chip), down to one batch of rows;
+    // every slice repeats its cluster's setup, which is small next to its rows
+    const int k = pick_k(s.W);
+    const uint32_t min_rows = k == 1 ? 8 : (k == 2 ? 4 : (k == 4 ? 2 : 1));
+    uint32_t rpu = s.G <= 64 ? s.G : 64;
+    while (rpu > min_rows && (g1 - g0 + 1) * ((s.G + rpu - 1) / rpu) < 16384) rpu = (rpu + 1) / 2;
     const uint32_t upg = (s.G + rpu - 1) / rpu;
     const uint64_t n_units = (g1 - g0 + 1) * upg;
     const uint64_t blocks = (n_units + kWavesPerBlock - 1) / kWavesPerBlock;
     const auto *p = reinterpret_cast<const uint32_t *>(payload);
     auto *o = static_cast<uint32_t *>(out);
     dim3 grid((unsigned)blocks), block(kBlock);
-    switch (pick_k(s.W)) {
+    switch (k) {
     case 1: hipLaunchKernelGGL((k_decompress<1, 4>), grid, block, 0, stream, s, p, pay_base, o, first, n, g0, n_units, upg, rpu); break;
     case 2: hipLaunchKernelGGL((k_decompress<2, 4>), grid, block, 0, stream, s, p, pay_base, o, first, n, g0, n_units, upg, rpu); break;
     case 4: hipLaunchKernelGGL((k_decompress<4, 2>), grid, block, 0, stream, s, p, pay_base, o, first, n, g0, n_units, upg, rpu); break;
