@@ -18,11 +18,18 @@ Also reported on the same JSON line:
                 duration from HIP events, against 8 TB/s; `traffic` comes from the
                 committed rocprofv3 counter summary of that kernel on that workload while
                 the kernel source is unchanged (else null); plus a plain 1 GiB device copy;
-  cpu_baseline  the CPU oracle (single thread, bit-serial) decoding a bounded sample of
-                one step's rows, in the same unit;
+  cpu_baseline  the CPU oracle (single thread, bit-serial) decoding the rows of whole steps
+                for about --cpu-seconds, in the same unit, plus an oracle compress sample
+                and the library's multi-threaded host compressor rate (context);
+  uncompressed_device  the same steps over the rows stored uncompressed (a stream whose
+                Masks are all 0, decoded by the same kernels): the uncompressed baseline;
   e2e           the PCIe-inclusive paths (payload in pinned host memory): host-packed
                 staging + DMA and GPU-initiated zero-copy reads; effective output GB/s
-                next to raw pinned H2D GB/s and the compression ratio of the bytes needed.
+                next to raw pinned H2D GB/s and the compression ratio of the bytes needed,
+                the speedup over moving the uncompressed rows the same way (the paper's
+                normalisation to uncompressed transfers, its Tab. 1), and the paper's mock
+                system (the same compressed bytes moved by one DMA per step and the rows
+                written, no decode; Sec. 6.4) as the ideal the path is compared with.
 """
 import argparse
 import hashlib
@@ -120,6 +127,41 @@ def raw_h2d_gbs(torch, nbytes, reps=5):
     return nbytes * reps / (s.elapsed_time(e) * 1e-3) / 1e9
 
 
+def identity_stream(rows, G):
+    """A valid stream holding the rows uncompressed: every cluster's Mask and Bitval are 0,
+    so each packed row is exactly the raw row (the stream format's raw case). Run through
+    the same placements and kernels it is the uncompressed-transfer baseline."""
+    n, L = rows.shape
+    ng = (n + G - 1) // G
+    meta_off, index_off = 64, 64 + ng * 2 * L
+    payload_off = index_off + 8 * (ng + 1)
+    s = np.zeros(payload_off + n * L, np.uint8)
+    hdr = s[:64]
+    hdr[:4] = np.frombuffer(b"IBP1", np.uint8)
+    hdr[4:16] = np.array([1, L, G], np.uint32).view(np.uint8)
+    hdr[16:32] = np.array([n, ng], np.uint64).view(np.uint8)
+    hdr[40:64] = np.array([meta_off, index_off, payload_off], np.uint64).view(np.uint8)
+    rows_per = np.full(ng, G, np.uint64)
+    rows_per[-1] = n - G * (ng - 1)
+    idx = np.zeros(ng + 1, np.uint64)
+    np.cumsum(rows_per * np.uint64(L), out=idx[1:])
+    s[index_off:payload_off] = idx.view(np.uint8)
+    s[payload_off:] = rows.reshape(-1)
+    return s
+
+
+def host_info():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": len(os.sched_getaffinity(0))}
+
+
 class Steps:
     """The per-step units of a workload: row-id batches (gathers) or row ranges (streams),
     with the algorithmic HBM bytes one launch over each must move."""
@@ -158,7 +200,44 @@ class Steps:
         return u if self.workload in GATHERS else np.arange(u[0], u[0] + u[1], dtype=np.int64)
 
 
-def pcie_legs(torch, ibp, args, stream, rows, steps, L, G, rb_of_group, index):
+def cpu_baseline(stream, rows, steps, last, L, G, seconds):
+    """The oracle on this host's cores (one thread): decode of exactly the rows of whole
+    steps, starting with the step the GPU ran last, until about `seconds` have passed; then
+    compress of the leading clusters of the tensor for about a third of that time."""
+    import oracle
+    t0 = time.perf_counter()
+    done_rows, done_steps, k = 0, 0, last
+    while True:
+        ids = steps.row_ids(k)
+        ref = oracle.decode_rows(stream, ids, L)
+        assert np.array_equal(ref, rows[ids]), "oracle decode"
+        done_rows += ids.size
+        done_steps += 1
+        k = (k + 1) % len(steps)
+        if time.perf_counter() - t0 >= seconds or done_steps >= 4 * len(steps):
+            break
+    dec_s = time.perf_counter() - t0
+    # compress: leading clusters, sized from a first cluster's time
+    n_groups = (rows.shape[0] + G - 1) // G
+    t = time.perf_counter()
+    oracle.compress(rows[:G], G)
+    per_group = max(time.perf_counter() - t, 1e-6)
+    ng = int(min(n_groups, max(1, seconds / 3 / per_group)))
+    m = min(rows.shape[0], ng * G)
+    t = time.perf_counter()
+    oracle.compress(rows[:m], G)
+    comp_s = time.perf_counter() - t
+    log(f"[bench] cpu oracle: decode {done_rows * L / dec_s / 1e6:.1f} MB/s over {done_steps} step(s); "
+        f"compress {m * L / comp_s / 1e6:.1f} MB/s over {ng} of {n_groups} clusters")
+    return {"value": round(done_rows * L / dec_s / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"bit-serial oracle decode of the rows of {done_steps} whole step(s) "
+                      f"({done_rows} rows, {dec_s:.1f} s, 1 thread)",
+            "compress": {"GBps": round(m * L / comp_s / 1e9, 6),
+                         "sample": f"leading {ng} of {n_groups} clusters ({m} rows, {comp_s:.1f} s, 1 thread)"},
+            "host": host_info()}
+
+
+def pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, G, rb_of_group, index):
     """The PCIe-inclusive legs (never `value`): the same steps with the payload in pinned
     host memory, (a) through host-packed staging + DMA on a side stream (host packing of
     the requested rows for gathers, whole cluster ranges for streams) and (b) read by the
@@ -170,14 +249,19 @@ def pcie_legs(torch, ibp, args, stream, rows, steps, L, G, rb_of_group, index):
     sel = [k % len(steps) for k in range(n_e2e)]
     out = torch.empty(max(steps.rows) * L, dtype=torch.uint8, device="cuda")
     out_total = sum(steps.rows[k] * L for k in sel)
-    if steps.workload in GATHERS:
-        need = sum(int(rb_of_group[steps.units[k] // G].sum()) + 8 * steps.rows[k] for k in sel)
-    else:
-        need = 0
-        for k in sel:
+    needs = {}
+    for k in set(sel):
+        if steps.workload in GATHERS:
+            needs[k] = int(rb_of_group[steps.units[k] // G].sum()) + 8 * steps.rows[k]
+        else:
             f, n = steps.units[k]
-            need += int(index[(f + n - 1) // G + 1] - index[f // G])
+            needs[k] = int(index[(f + n - 1) // G + 1] - index[f // G])
+    need = sum(needs[k] for k in sel)
     cr = out_total / need
+
+    def mock_step(k):
+        dev_buf[:needs[k]].copy_(host_buf[:needs[k]], non_blocking=True)
+        out[:steps.rows[k] * L].fill_(0)
     res = {"raw_h2d_GBps_1GiB": round(raw, 2), "steps": n_e2e, "cr": round(cr, 3)}
 
     def run(h, k):
@@ -187,9 +271,10 @@ def pcie_legs(torch, ibp, args, stream, rows, steps, L, G, rb_of_group, index):
             f, n = steps.units[k]
             ibp.ibp_decompress(h, f, n, out)
 
-    for mode, flags in (("staged_dma", ibp.IBP_OPEN_PAYLOAD_HOST), ("zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)):
-        h = ibp.ibp_open(stream, 0, flags)
-        run(h, sel[0])
+    def leg(src, flags, check):
+        h = ibp.ibp_open(src, 0, flags)
+        for k in sel[:3]:
+            run(h, k)
         torch.cuda.synchronize()
         ibp.ibp_reset_stats(h)
         t = time.perf_counter()
@@ -200,13 +285,40 @@ def pcie_legs(torch, ibp, args, stream, rows, steps, L, G, rb_of_group, index):
         st = ibp.ibp_get_stats(h)
         last = sel[-1]
         got = out[:steps.rows[last] * L].cpu().numpy().reshape(-1, L)
-        assert np.array_equal(got, rows[steps.row_ids(last)]), mode
+        assert np.array_equal(got, rows[steps.row_ids(last)]), check
         ibp.ibp_close(h)
+        return dt, st
+
+    # the paper's mock system: the same compressed bytes cross PCIe (one pinned DMA per step)
+    # and the uncompressed rows are written, with no decode
+    host_buf = torch.empty(max(needs.values()), dtype=torch.uint8, pin_memory=True)
+    dev_buf = torch.empty(max(needs.values()), dtype=torch.uint8, device="cuda")
+    for k in sel[:3]:
+        mock_step(k)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    for k in sel:
+        mock_step(k)
+    torch.cuda.synchronize()
+    dt_mock = time.perf_counter() - t
+    res["mock"] = {"GBps": round(out_total / dt_mock / 1e9, 2),
+                   "raw_h2d_GBps_batch": round(need / dt_mock / 1e9, 2)}
+    log(f"[bench] e2e mock (compressed bytes moved, rows written, no decode): {out_total / dt_mock / 1e9:.1f} GB/s; "
+        f"raw H2D at the batch's size {need / dt_mock / 1e9:.1f} GB/s")
+    del host_buf, dev_buf
+    for mode, flags in (("staged_dma", ibp.IBP_OPEN_PAYLOAD_HOST), ("zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)):
+        dt, st = leg(stream, flags, mode)
+        dt_raw, _ = leg(ident, flags, mode + " uncompressed")
         eff = out_total / dt / 1e9
         res[mode] = {"effective_GBps": round(eff, 2), "effective_over_cr_raw": round(eff / (cr * raw), 3),
+                     "effective_over_cr_minus_0p1_raw": round(eff / ((cr - 0.1) * raw), 3),
+                     "effective_over_mock": round(dt_mock / dt, 3),
+                     "uncompressed_GBps": round(out_total / dt_raw / 1e9, 2),
+                     "speedup_vs_uncompressed": round(dt_raw / dt, 3),
                      "host_pack_ms_per_step": round(st["host_pack_ns"] / n_e2e / 1e6, 3)}
         log(f"[bench] e2e {mode}: {eff:.1f} GB/s effective ({eff / (cr * raw):.2f} of CR x raw, "
-            f"raw {raw:.1f} GB/s, CR {cr:.2f})")
+            f"raw {raw:.1f} GB/s, CR {cr:.2f}); uncompressed rows through the same path "
+            f"{out_total / dt_raw / 1e9:.1f} GB/s -> speedup {dt_raw / dt:.2f}x")
     return res
 
 
@@ -276,7 +388,8 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     out_bytes = sum(steps.rows[(Wm + k) % len(steps)] * L for k in range(K))
-    kern_ms = float(np.mean([s.elapsed_time(e) for s, e in ev]))
+    kern_all = np.array([s.elapsed_time(e) for s, e in ev])
+    kern_ms = float(np.mean(kern_all))
     alg_avg = float(np.mean([steps.alg[(Wm + k) % len(steps)] for k in range(K)]))
     achieved = alg_avg / (kern_ms * 1e-3) / 1e9
     value = out_bytes / wall / 1e9
@@ -287,6 +400,23 @@ def main():
         sys.exit(1)
     assert ibp.ibp_device_errors(h) == 0
     ibp.ibp_close(h)
+    # the same steps over the rows stored uncompressed (Mask = 0 everywhere), same kernels
+    ident = identity_stream(rows, G)
+    hu = ibp.ibp_open(ident, 0, ibp.IBP_OPEN_PAYLOAD_DEVICE)
+    h = hu
+    for k in range(Wm):
+        step(k)
+    torch.cuda.synchronize()
+    t0u = time.perf_counter()
+    for k in range(K):
+        step(Wm + k)
+    torch.cuda.synchronize()
+    wall_u = time.perf_counter() - t0u
+    got = out[:steps.rows[last] * L].cpu().numpy().reshape(-1, L)
+    assert np.array_equal(got, rows[steps.row_ids(last)]), "uncompressed baseline"
+    ibp.ibp_close(hu)
+    log(f"[bench] same steps over uncompressed rows (device-resident): {out_bytes / wall_u / 1e9:.1f} GB/s "
+        f"-> compressed is {wall_u / wall:.2f}x the uncompressed speed")
     copy_gbs = d2d_copy_gbs(torch)
     traffic = measured_traffic(wl)
     log(f"[bench] {K} steps in {wall * 1e3:.2f} ms: {value:.1f} GB/s decompressed; kernel {kern_ms * 1e3:.1f} us "
@@ -295,25 +425,12 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        import oracle
-        ids = steps.row_ids(last)
-        probe = ids[:min(400, ids.size)]
-        t = time.perf_counter()
-        oracle.decode_rows(stream, probe, L)
-        per_row = (time.perf_counter() - t) / probe.size
-        m = int(min(ids.size, max(probe.size, args.cpu_seconds / per_row)))
-        t = time.perf_counter()
-        ref = oracle.decode_rows(stream, ids[:m], L)
-        cpu_s = time.perf_counter() - t
-        assert np.array_equal(ref, rows[ids[:m]])
-        cpu = {"value": round(m * L / cpu_s / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
-               "sample": f"bit-serial oracle decode of the first {m} of {ids.size} rows of one step "
-                         f"({cpu_s:.1f} s, 1 thread)"}
-        log(f"[bench] cpu oracle: {cpu['value'] * 1e3:.2f} MB/s over {m} rows")
+        cpu = cpu_baseline(stream, rows, steps, last, L, G, args.cpu_seconds)
+        cpu["host_compressor"] = {"GBps": round(cfg.n_rows * L / compress_s / 1e9, 3), "threads": threads}
 
     e2e = None
     if not args.no_e2e:
-        e2e = pcie_legs(torch, ibp, args, stream, rows, steps, L, G, rb_of_group, index)
+        e2e = pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, G, rb_of_group, index)
 
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": Wm,
@@ -326,7 +443,11 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "kernel": kernel_name(wl, W), "kernel_us": round(kern_ms * 1e3, 2),
+                     "kernel_us_median": round(float(np.median(kern_all)) * 1e3, 2),
+                     "kernel_us_min": round(float(kern_all.min()) * 1e3, 2),
                      "algorithmic_bytes_per_launch": int(alg_avg), "d2d_copy_GBps": round(copy_gbs, 1)},
+        "uncompressed_device": {"GBps": round(out_bytes / wall_u / 1e9, 2),
+                                "speedup_of_compressed": round(wall_u / wall, 3)},
         "cpu_baseline": cpu,
         "e2e": e2e,
     }

@@ -3,6 +3,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <functional>
 #include <string>
 
 #include "ibp.h"
@@ -37,5 +38,22 @@ inline uint64_t packed_row_bytes(uint32_t row_bytes, uint64_t mask_popcount) {
 }
 
 int online_cpus();
+
+// Persistent worker pool (threads - 1 workers plus the calling thread).
+class Pool {
+public:
+    explicit Pool(int threads);
+    ~Pool();
+    Pool(const Pool &) = delete;
+    Pool &operator=(const Pool &) = delete;
+    int size() const;
+    // Run fn(lo, hi) over [0, n) in blocks of `block` on every worker and the caller;
+    // returns once every block has run. One caller at a time.
+    void run(uint64_t n, uint64_t block, const std::function<void(uint64_t, uint64_t)> &fn);
+
+private:
+    struct State;
+    State *st_;
+};
 
 }  // namespace ibp

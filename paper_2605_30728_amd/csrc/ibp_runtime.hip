@@ -12,12 +12,12 @@
 // past its last packed byte.
 //
 // PCIe path (IBP_OPEN_PAYLOAD_HOST): the packed payload lives in library-owned pinned
-// host memory. Two device staging buffers alternate; for chunk k the side copy stream
-// first waits until the kernel that read buffer k%2 two chunks ago has finished, copies
-// the chunk in, and records an event that the caller's stream waits on before the
-// decode kernel (the paper overlaps CPU memory reads with decoding, Sec. 4.3; here the
-// overlap is between DMA of chunk k+1 and decode of chunk k). For gathers the host first
-// packs the selected packed rows, their ids and staged offsets into pinned staging
+// host memory. kStages device staging buffers rotate; for chunk k the side copy stream
+// first waits until the kernel that last read buffer k%kStages has finished, copies the
+// chunk in, and records an event that the caller's stream waits on before the decode
+// kernel (the paper overlaps CPU memory reads with decoding, Sec. 4.3; here the overlap
+// is between DMA of chunk k+1 and decode of chunk k). For gathers the host first packs
+// the selected packed rows, their clusters and staged offsets into pinned staging
 // (multi-threaded), which is the host half of the paper's lookup + transfer.
 #include <algorithm>
 #include <atomic>
@@ -41,84 +41,25 @@ namespace {
 constexpr uint64_t kSlack = 256;                 // readable bytes past any payload end
 constexpr uint64_t kStageBytes = 16ull << 20;    // one staging buffer
 constexpr int kStages = 3;                        // staging buffers in rotation
+constexpr int kIdSlots = 2;                       // host-id buffers in rotation
+constexpr uint64_t kBlk = 256;                    // rows per host packing task (a chunk
+                                                  // holds tens of them, for 16 threads)
 
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
 // Best-effort calls (cleanup, device restore) whose status is deliberately ignored.
 inline void ignore(hipError_t) {}
 
-// A small persistent worker pool for host packing and large host copies.
-class Pool {
-public:
-    explicit Pool(int n) {
-        for (int i = 0; i < n - 1; ++i) workers_.emplace_back([this] { loop(); });
+// Host wait for an event by polling: the staging pipeline waits for copies that are
+// normally about to finish, and polling resumes within microseconds where a blocking
+// synchronize can sleep much longer.
+hipError_t wait_event(hipEvent_t e) {
+    for (;;) {
+        const hipError_t r = hipEventQuery(e);
+        if (r != hipErrorNotReady) return r;
+        std::this_thread::yield();
     }
-    ~Pool() {
-        {
-            std::lock_guard<std::mutex> g(mu_);
-            stop_ = true;
-            ++gen_;
-        }
-        cv_.notify_all();
-        for (auto &t : workers_) t.join();
-    }
-    int size() const { return (int)workers_.size() + 1; }
-    // Run fn(lo, hi) over [0, n) in blocks of `block` on every worker and the caller.
-    void run(uint64_t n, uint64_t block, const std::function<void(uint64_t, uint64_t)> &fn) {
-        if (n == 0) return;
-        if (workers_.empty() || n <= block) {
-            fn(0, n);
-            return;
-        }
-        {
-            std::lock_guard<std::mutex> g(mu_);
-            fn_ = &fn;
-            n_ = n;
-            block_ = block;
-            next_.store(0);
-            pending_ = (int)workers_.size();
-            ++gen_;
-        }
-        cv_.notify_all();
-        work();
-        std::unique_lock<std::mutex> lk(mu_);
-        done_.wait(lk, [this] { return pending_ == 0; });
-        fn_ = nullptr;
-    }
-
-private:
-    void work() {
-        for (;;) {
-            uint64_t lo = next_.fetch_add(block_);
-            if (lo >= n_) break;
-            (*fn_)(lo, std::min(n_, lo + block_));
-        }
-    }
-    void loop() {
-        uint64_t seen = 0;
-        for (;;) {
-            {
-                std::unique_lock<std::mutex> lk(mu_);
-                cv_.wait(lk, [&] { return gen_ != seen; });
-                seen = gen_;
-                if (stop_) return;
-            }
-            work();
-            {
-                std::lock_guard<std::mutex> g(mu_);
-                if (--pending_ == 0) done_.notify_one();
-            }
-        }
-    }
-    std::vector<std::thread> workers_;
-    std::mutex mu_;
-    std::condition_variable cv_, done_;
-    const std::function<void(uint64_t, uint64_t)> *fn_ = nullptr;
-    uint64_t n_ = 0, block_ = 1, gen_ = 0;
-    std::atomic<uint64_t> next_{0};
-    int pending_ = 0;
-    bool stop_ = false;
-};
+}
 
 }  // namespace
 }  // namespace ibp
@@ -135,11 +76,13 @@ struct ibp_handle {
     uint8_t *d_payload = nullptr;
     const uint8_t *k_payload = nullptr;   // what the kernels read: d_payload or the pinned host payload
     unsigned long long *d_err = nullptr;
-    // host ids of gathers over a device payload
-    int64_t *h_ids = nullptr, *d_ids = nullptr;
-    uint64_t ids_cap = 0;
-    hipEvent_t ev_ids = nullptr;
-    bool ids_pending = false;
+    // host ids of gathers over a device or zero-copy payload: two slots alternate, so the
+    // ids of call k+1 are staged while the kernel of call k still reads slot k%2
+    int64_t *h_ids[kIdSlots] = {}, *d_ids[kIdSlots] = {};
+    uint64_t ids_cap[kIdSlots] = {};
+    hipEvent_t ev_ids_free[kIdSlots] = {};
+    bool ids_used[kIdSlots] = {};
+    int next_ids = 0;
     // PCIe path
     uint8_t *h_payload = nullptr;
     std::vector<uint64_t> h_off;
@@ -153,7 +96,8 @@ struct ibp_handle {
     bool stage_used[kStages] = {};
     int next_stage = 0;
     std::vector<uint32_t> req_g, req_rb;   // per-request cluster and packed size (host gathers)
-    std::vector<uint64_t> blk_off;         // per-block staged byte offsets (host gathers)
+    std::vector<uint64_t> blk_off;         // packed bytes of every packing block (host gathers)
+    std::vector<uint64_t> chunk_off;       // staged byte offset of every block of one chunk
     Pool *pool = nullptr;
     std::atomic<int> busy{0};
     ibp_stats stats{};
@@ -212,8 +156,11 @@ void free_handle(ibp_handle *h) {
     ignore(hipFree(h->d_index));
     ignore(hipFree(h->d_payload));
     ignore(hipFree(h->d_err));
-    ignore(hipFree(h->d_ids));
-    if (h->h_ids) ignore(hipHostFree(h->h_ids));
+    for (int j = 0; j < kIdSlots; ++j) {
+        ignore(hipFree(h->d_ids[j]));
+        if (h->h_ids[j]) ignore(hipHostFree(h->h_ids[j]));
+        if (h->ev_ids_free[j]) ignore(hipEventDestroy(h->ev_ids_free[j]));
+    }
     if (h->h_payload) ignore(hipHostFree(h->h_payload));
     for (int b = 0; b < kStages; ++b) {
         if (h->h_stage[b]) ignore(hipHostFree(h->h_stage[b]));
@@ -221,30 +168,27 @@ void free_handle(ibp_handle *h) {
         if (h->ev_copied[b]) ignore(hipEventDestroy(h->ev_copied[b]));
         if (h->ev_free[b]) ignore(hipEventDestroy(h->ev_free[b]));
     }
-    if (h->ev_ids) ignore(hipEventDestroy(h->ev_ids));
     if (h->copy_stream) ignore(hipStreamDestroy(h->copy_stream));
     delete h->pool;
     delete h;
 }
 
-// Ensure the pinned + device id buffers of a handle hold n ids.
-ibp_status ensure_ids(ibp_handle *h, uint64_t n) {
-    if (n <= h->ids_cap) return IBP_OK;
-    if (h->ids_pending) {
-        IBP_HIP(h, hipEventSynchronize(h->ev_ids));
-        h->ids_pending = false;
-    }
-    uint64_t cap = std::max<uint64_t>(n, 2 * h->ids_cap);
-    if (h->h_ids) ignore(hipHostFree(h->h_ids));
-    ignore(hipFree(h->d_ids));
-    h->h_ids = nullptr;
-    h->d_ids = nullptr;
-    h->ids_cap = 0;
-    if (hipHostMalloc((void **)&h->h_ids, cap * 8, hipHostMallocDefault) != hipSuccess)
+// Claim id slot j for n ids: its last kernel must have finished with it (host wait, needed
+// anyway before the pinned half is rewritten), and the buffers must hold n ids.
+ibp_status claim_ids(ibp_handle *h, int j, uint64_t n) {
+    if (h->ids_used[j]) IBP_HIP(h, wait_event(h->ev_ids_free[j]));
+    if (n <= h->ids_cap[j]) return IBP_OK;
+    uint64_t cap = std::max<uint64_t>(n, 2 * h->ids_cap[j]);
+    if (h->h_ids[j]) ignore(hipHostFree(h->h_ids[j]));
+    ignore(hipFree(h->d_ids[j]));
+    h->h_ids[j] = nullptr;
+    h->d_ids[j] = nullptr;
+    h->ids_cap[j] = 0;
+    if (hipHostMalloc((void **)&h->h_ids[j], cap * 8, hipHostMallocDefault) != hipSuccess)
         return fail(IBP_ENOMEM, "pinned allocation for row ids failed");
-    if (hipMalloc((void **)&h->d_ids, cap * 8) != hipSuccess)
+    if (hipMalloc((void **)&h->d_ids[j], cap * 8) != hipSuccess)
         return fail(IBP_ENOMEM, "device allocation for row ids failed");
-    h->ids_cap = cap;
+    h->ids_cap[j] = cap;
     return IBP_OK;
 }
 
@@ -285,7 +229,7 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
 // kernel that last read it (device wait on the copy stream).
 ibp_status claim_stage(ibp_handle *h, int b, bool host_side_too) {
     if (h->stage_used[b]) {
-        if (host_side_too) IBP_HIP(h, hipEventSynchronize(h->ev_copied[b]));
+        if (host_side_too) IBP_HIP(h, wait_event(h->ev_copied[b]));
         IBP_HIP(h, hipStreamWaitEvent(h->copy_stream, h->ev_free[b], 0));
     }
     return IBP_OK;
@@ -298,21 +242,36 @@ ibp_status claim_stage(ibp_handle *h, int b, bool host_side_too) {
 ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, uint8_t *d_out, hipStream_t s) {
     const uint64_t L = h->d.row_bytes, G = h->d.group_rows;
     const uint64_t magic = dev::div_magic((uint32_t)G);
+    // rows per chunk: as many as one staging buffer holds (8 B of tables + the largest packed
+    // row each), in whole packing blocks. Consecutive calls overlap through the rotating
+    // buffers (call k+1 packs while call k's chunk crosses PCIe); cutting a call into
+    // smaller chunks measured slower, since every chunk costs a DMA and a launch.
+    const uint64_t row_max = 8 + (uint64_t)h->max_rb;
+    const uint64_t cap_rows = std::max<uint64_t>(1, (kStageBytes - 64) / row_max);
+    const uint64_t per_chunk = cap_rows >= kBlk ? cap_rows / kBlk * kBlk : cap_rows;
+    const uint64_t blk = std::min(kBlk, per_chunk);   // per_chunk is a multiple of blk
+    // one pass over the ids: cluster and packed size of every request, and the packed
+    // bytes of every block
+    const uint64_t nblk_all = (n + blk - 1) / blk;
     h->req_g.resize(n);
     h->req_rb.resize(n);
+    h->blk_off.assign(nblk_all + 1, 0);
     uint32_t *rg = h->req_g.data(), *rrb = h->req_rb.data();
+    uint64_t *bs = h->blk_off.data();
     const uint32_t *grb = h->h_rb.data();
-    h->pool->run(n, 8192, [&](uint64_t lo, uint64_t hi) {
-        for (uint64_t i = lo; i < hi; ++i) {
-            const uint64_t id = (uint64_t)ids[i];
-            const uint64_t g = G == 1 ? id : (uint64_t)(((unsigned __int128)id * magic) >> 64);
-            rg[i] = (uint32_t)g;
-            rrb[i] = grb[g];
+    h->pool->run(nblk_all, 1, [&](uint64_t lo, uint64_t hi) {
+        for (uint64_t k = lo; k < hi; ++k) {
+            uint64_t sum = 0;
+            for (uint64_t i = k * blk, e = std::min(n, i + blk); i < e; ++i) {
+                const uint64_t id = (uint64_t)ids[i];
+                const uint64_t g = G == 1 ? id : (uint64_t)(((unsigned __int128)id * magic) >> 64);
+                rg[i] = (uint32_t)g;
+                rrb[i] = grb[g];
+                sum += grb[g];
+            }
+            bs[k + 1] = sum;
         }
     });
-    // fixed rows per chunk so that any chunk fits: 8 B of tables + the largest packed row
-    const uint64_t per_chunk = std::max<uint64_t>(1, (kStageBytes - 64) / (8 + (uint64_t)h->max_rb));
-    constexpr uint64_t kBlk = 2048;
     for (uint64_t i0 = 0; i0 < n; i0 += per_chunk) {
         const uint64_t nc = std::min(per_chunk, n - i0);
         const int b = h->next_stage;
@@ -324,28 +283,21 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
         uint32_t *sg = reinterpret_cast<uint32_t *>(stg);
         uint32_t *soff = sg + nc;
         uint8_t *pay = stg + 8 * nc;
-        // staged offsets: block sums in parallel, a short scan over blocks, then every
-        // block writes its tables and copies its rows (prefetching a few rows ahead,
-        // since each row is a random read of ~rb bytes from host memory)
-        const uint64_t nblk = (nc + kBlk - 1) / kBlk;
-        h->blk_off.assign(nblk + 1, 0);
-        uint64_t *bo = h->blk_off.data();
-        h->pool->run(nblk, 1, [&](uint64_t lo, uint64_t hi) {
-            for (uint64_t k = lo; k < hi; ++k) {
-                uint64_t sum = 0;
-                const uint64_t a = i0 + k * kBlk, e = std::min(i0 + nc, a + kBlk);
-                for (uint64_t i = a; i < e; ++i) sum += rrb[i];
-                bo[k + 1] = sum;
-            }
-        });
-        for (uint64_t k = 0; k < nblk; ++k) bo[k + 1] += bo[k];
+        // staged offsets: an exclusive scan over this chunk's block sums, then every block
+        // writes its tables and copies its rows (prefetching a few rows ahead, since each
+        // row is a random read of ~rb bytes from host memory)
+        const uint64_t k0 = i0 / blk, nblk = (nc + blk - 1) / blk;
+        h->chunk_off.resize(nblk + 1);
+        uint64_t *bo = h->chunk_off.data();
+        bo[0] = 0;
+        for (uint64_t k = 0; k < nblk; ++k) bo[k + 1] = bo[k] + bs[k0 + k + 1];
         const uint64_t total_pay = bo[nblk];
         const uint8_t *src_base = h->h_payload;
         const uint64_t *goff = h->h_off.data();
         h->pool->run(nblk, 1, [&](uint64_t lo, uint64_t hi) {
-            constexpr uint64_t kAhead = 8;
+            constexpr uint64_t kAhead = 12;
             for (uint64_t k = lo; k < hi; ++k) {
-                const uint64_t a = i0 + k * kBlk, e = std::min(i0 + nc, a + kBlk);
+                const uint64_t a = i0 + k * blk, e = std::min(i0 + nc, a + blk);
                 uint64_t o = bo[k];
                 auto src_of = [&](uint64_t i) {
                     const uint64_t g = rg[i], r = (uint64_t)ids[i] - g * G;
@@ -452,8 +404,9 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
             h->k_payload = static_cast<const uint8_t *>(dp);
         }
     }
-    if (hipEventCreateWithFlags(&h->ev_ids, hipEventDisableTiming) != hipSuccess)
-        return bail(fail(IBP_EHIP, "event creation failed"));
+    for (int j = 0; j < kIdSlots; ++j)
+        if (hipEventCreateWithFlags(&h->ev_ids_free[j], hipEventDisableTiming) != hipSuccess)
+            return bail(fail(IBP_EHIP, "event creation failed"));
     if (hipDeviceSynchronize() != hipSuccess) return bail(fail(IBP_EHIP, "upload did not complete"));
     h->ds.meta = h->d_meta;
     h->ds.index = h->d_index;
@@ -535,14 +488,15 @@ ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t
     hipStream_t s = static_cast<hipStream_t>(stream);
     const uint64_t L = d.row_bytes;
     if (h->flags != IBP_OPEN_PAYLOAD_HOST) {
-        st = ensure_ids(h, n_ids);
+        const int j = h->next_ids;
+        st = claim_ids(h, j, n_ids);
         if (st != IBP_OK) return st;
-        if (h->ids_pending) IBP_HIP(h, hipEventSynchronize(h->ev_ids));
-        std::memcpy(h->h_ids, row_ids, n_ids * 8);
-        IBP_HIP(h, hipMemcpyAsync(h->d_ids, h->h_ids, n_ids * 8, hipMemcpyHostToDevice, s));
-        IBP_HIP(h, dev::launch_gather(h->ds, h->k_payload, h->d_ids, nullptr, nullptr, n_ids, d_out, h->d_err, s));
-        IBP_HIP(h, hipEventRecord(h->ev_ids, s));
-        h->ids_pending = true;
+        h->next_ids = (j + 1) % kIdSlots;
+        std::memcpy(h->h_ids[j], row_ids, n_ids * 8);
+        IBP_HIP(h, hipMemcpyAsync(h->d_ids[j], h->h_ids[j], n_ids * 8, hipMemcpyHostToDevice, s));
+        IBP_HIP(h, dev::launch_gather(h->ds, h->k_payload, h->d_ids[j], nullptr, nullptr, n_ids, d_out, h->d_err, s));
+        IBP_HIP(h, hipEventRecord(h->ev_ids_free[j], s));
+        h->ids_used[j] = true;
         h->stats.h2d_bytes += n_ids * 8;
     } else {
         st = gather_host_payload(h, row_ids, n_ids, static_cast<uint8_t *>(d_out), s);

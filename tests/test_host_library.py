@@ -169,3 +169,14 @@ def test_big_row_tiled_streams_match():
     """Rows wider than one wave tile (more than 512 words) still match the oracle."""
     rows = structured_rows("sparse", 70, 4 * 1500, seed=9)
     assert np.array_equal(ibp.ibp_compress(rows, 32), oracle.compress(rows, 32))
+
+
+def test_identity_stream_is_valid_and_raw():
+    """The uncompressed baseline stream of bench.py (every Mask 0) validates and decodes,
+    bit by bit through the oracle, to exactly the raw rows."""
+    import bench
+    rows = structured_rows("floats", 70, 64, seed=21)
+    s = bench.identity_stream(rows, 16)
+    d = ibp.ibp_describe(s)
+    assert d["payload_bytes"] == rows.nbytes and d["n_groups"] == 5
+    assert np.array_equal(oracle.decompress(s, 70, 64), rows)
