@@ -29,7 +29,7 @@ Also reported on the same JSON line:
                 the speedup over moving the uncompressed rows the same way (the paper's
                 normalisation to uncompressed transfers, its Tab. 1), and the paper's mock
                 system (the same compressed bytes moved by one DMA per step and the rows
-                written, no decode; Sec. 6.4) as the ideal the path is compared with.
+                written, no decode; Sec. 6.1) as the ideal the path is compared with.
 """
 import argparse
 import hashlib
