@@ -30,6 +30,10 @@ Also reported on the same JSON line:
                 normalisation to uncompressed transfers, its Tab. 1), and the paper's mock
                 system (the same compressed bytes moved by one DMA per step and the rows
                 written, no decode; Sec. 6.1) as the ideal the path is compared with.
+
+`--micro` runs the paper's decompression-overhead microbenchmark instead (tensors of
+256 B / 1 KB / 4 KB at 10-90% space savings, PCIe paths normalised to the mock system)
+and prints one JSON line holding every point.
 """
 import argparse
 import hashlib
@@ -322,6 +326,87 @@ def pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, G, rb_of_group, i
     return res
 
 
+MICRO_SIZES = (256, 1024, 4096)
+MICRO_SAVINGS = (0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7, 0.8, 0.9)
+
+
+def micro(args):
+    """The paper's decompression-overhead microbenchmark (Sec. 6.1, Fig. decompression_micro):
+    for tensors of 256 B, 1 KB and 4 KB and target space savings of 10-90%, n tensors
+    with that many fixed bits (clusters of 32 tensors) sit compressed in pinned host
+    memory; one step transfers and decompresses all of them into HBM (ibp_decompress over
+    the whole set). Throughput is normalised to the mock system: one DMA of the same
+    compressed bytes plus a write of the uncompressed tensors, with no decode."""
+    import torch
+    import paper_2605_30728_amd as ibp
+    from workloads import micro_rows
+    n, iters, G = args.micro_tensors, args.micro_iters, 32
+    raw = raw_h2d_gbs(torch, 1 << 30)
+
+    def timed(fn):
+        # median over iterations of the time between completions (each iteration is
+        # enqueued behind the previous one), so a host stall in one iteration does not
+        # decide the point
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)]
+        ev[0].record()
+        for k in range(iters):
+            fn()
+            ev[k + 1].record()
+        torch.cuda.synchronize()
+        return float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(iters)])) * 1e-3
+
+    def point(L, target, out):
+        rows = micro_rows(n, L, target)
+        stream = ibp.ibp_compress(rows, G)
+        d = ibp.ibp_describe(stream)
+        pay = max(d["payload_bytes"], 1)
+        ref = torch.from_numpy(rows.reshape(-1)).cuda()
+        host_buf = torch.empty(pay, dtype=torch.uint8, pin_memory=True)
+        dev_buf = torch.empty(pay, dtype=torch.uint8, device="cuda")
+
+        def mock():
+            dev_buf.copy_(host_buf, non_blocking=True)
+            out.fill_(0)
+        t_mock = timed(mock)
+        del host_buf, dev_buf
+        pt = {"tensor_bytes": L, "target_savings": target,
+              "savings": round(1 - d["payload_bytes"] / (n * L), 4),
+              "mock_GBps": round(n * L / t_mock / 1e9, 2)}
+        for mode, flags in (("zero_copy", ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY),
+                            ("staged_dma", ibp.IBP_OPEN_PAYLOAD_HOST)):
+            h = ibp.ibp_open(stream, 0, flags)
+            dt = timed(lambda: ibp.ibp_decompress(h, 0, n, out))
+            ok = bool(torch.equal(out, ref))
+            ibp.ibp_close(h)
+            if not ok:
+                log(f"[micro] ERROR: {mode} L={L} savings={target}: output differs from the tensors")
+                sys.exit(1)
+            pt[mode] = {"GBps": round(n * L / dt / 1e9, 2), "frac_of_mock": round(t_mock / dt, 3)}
+        return pt
+
+    sizes = [int(x) for x in args.micro_sizes.split(",")]
+    savings = [float(x) for x in args.micro_savings.split(",")]
+    points = []
+    for L in sizes:
+        out = torch.empty(n * L, dtype=torch.uint8, device="cuda")
+        if L == sizes[0]:
+            point(L, savings[0], out)      # warm-up pass (first pinned buffers, first launches)
+        for target in savings:
+            pt = point(L, target, out)
+            log(f"[micro] {L:5d} B, savings {pt['savings']:.3f}: mock {pt['mock_GBps']:.1f} GB/s; "
+                f"zero-copy {pt['zero_copy']['GBps']:.1f} ({pt['zero_copy']['frac_of_mock']:.2f} of mock); "
+                f"staged {pt['staged_dma']['GBps']:.1f} ({pt['staged_dma']['frac_of_mock']:.2f})")
+            points.append(pt)
+        del out
+    print(json.dumps({"metric": "decompression throughput relative to the no-decode mock system",
+                      "unit": "fraction of mock", "n_gpus": 1, "tensors": n, "iterations": iters,
+                      "group_rows": G, "raw_h2d_GBps_1GiB": round(raw, 2), "data": "synthetic",
+                      "points": points}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -332,11 +417,22 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-e2e", action="store_true")
     ap.add_argument("--e2e-steps", type=int, default=20)
+    ap.add_argument("--micro", action="store_true",
+                    help="run the decompression-overhead microbenchmark instead (one JSON line with every point)")
+    ap.add_argument("--micro-tensors", type=int, default=100000)
+    ap.add_argument("--micro-iters", type=int, default=100)
+    ap.add_argument("--micro-sizes", default=",".join(map(str, MICRO_SIZES)),
+                    help="comma-separated tensor sizes in bytes")
+    ap.add_argument("--micro-savings", default=",".join(map(str, MICRO_SAVINGS)),
+                    help="comma-separated target space savings")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(clusters shard by row range with no exchange between GPUs)", file=sys.stderr)
         sys.exit(2)
+    if args.micro:
+        micro(args)
+        return
 
     import torch
     import paper_2605_30728_amd as ibp

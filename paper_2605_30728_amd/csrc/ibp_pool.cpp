@@ -1,10 +1,10 @@
 // Persistent host worker pool of the runtime (host packing of gathers, large host copies).
 //
 // A PCIe gather call runs the pool once per staging chunk, so the time to start a run
-// is on the critical path. Workers therefore spin on the generation counter for a short
-// while after each run (a run then starts within about a microsecond) and only then
-// sleep on a condition variable; the caller takes part in every run and spins until the
-// workers have finished it.
+// is on the critical path. Workers therefore spin on the generation counter for a short,
+// time-bounded while after each run (a run then starts within about a microsecond) and
+// only then sleep on a condition variable; the caller takes part in every run and waits
+// for the workers to finish it.
 #include <atomic>
 #include <chrono>
 #include <condition_variable>
@@ -19,7 +19,23 @@
 namespace ibp {
 
 namespace {
-constexpr int kSpinRounds = 1 << 14;   // pause rounds before a worker sleeps (~0.1-0.5 ms)
+// How long a worker spins for the next run before it sleeps: long enough to bridge the
+// host work between the chunks of one call and between back-to-back calls, short enough
+// not to take CPU time from the HIP runtime's own threads for long.
+constexpr auto kSpin = std::chrono::microseconds(200);
+
+// Spin until pred() holds or the spin time is over; returns pred().
+template <class P>
+bool spin_until(P pred) {
+    const auto end = std::chrono::steady_clock::now() + kSpin;
+    for (;;) {
+        for (int i = 0; i < 64; ++i) {
+            if (pred()) return true;
+            _mm_pause();
+        }
+        if (std::chrono::steady_clock::now() >= end) return pred();
+    }
+}
 }
 
 struct Pool::State {
@@ -44,11 +60,8 @@ struct Pool::State {
     void loop() {
         uint64_t seen = 0;
         for (;;) {
+            spin_until([&] { return gen.load(std::memory_order_acquire) != seen; });
             uint64_t g = gen.load(std::memory_order_acquire);
-            for (int i = 0; g == seen && i < kSpinRounds; ++i) {
-                _mm_pause();
-                g = gen.load(std::memory_order_acquire);
-            }
             if (g == seen) {
                 std::unique_lock<std::mutex> lk(mu);
                 cv.wait(lk, [&] { return gen.load(std::memory_order_acquire) != seen; });
@@ -98,12 +111,8 @@ void Pool::run(uint64_t n, uint64_t block, const std::function<void(uint64_t, ui
     }
     s.cv.notify_all();
     s.work();
-    for (uint64_t i = 0; s.pending.load(std::memory_order_acquire) != 0; ++i) {
-        if (i < (uint64_t)kSpinRounds)
-            _mm_pause();
-        else
-            std::this_thread::yield();
-    }
+    while (!spin_until([&] { return s.pending.load(std::memory_order_acquire) == 0; }))
+        std::this_thread::yield();
     s.fn = nullptr;
 }
 

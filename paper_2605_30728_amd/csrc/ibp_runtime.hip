@@ -39,7 +39,7 @@ namespace ibp {
 namespace {
 
 constexpr uint64_t kSlack = 256;                 // readable bytes past any payload end
-constexpr uint64_t kStageBytes = 16ull << 20;    // one staging buffer
+constexpr uint64_t kStageBytes = 64ull << 20;    // one staging buffer
 constexpr int kStages = 3;                        // staging buffers in rotation
 constexpr int kIdSlots = 2;                       // host-id buffers in rotation
 constexpr uint64_t kBlk = 256;                    // rows per host packing task (a chunk
@@ -437,32 +437,42 @@ ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, vo
     if (h->flags != IBP_OPEN_PAYLOAD_HOST) {
         IBP_HIP(h, dev::launch_decompress(h->ds, h->k_payload, 0, d_out, first_row, n_rows, s));
     } else {
-        // chunks of whole groups whose packed bytes fit one staging buffer
+        // chunks of consecutive rows whose packed bytes fit one staging buffer: the packed
+        // rows of any row range are one contiguous byte range of the payload (clusters back
+        // to back, rows of a cluster back to back), so exactly those bytes cross PCIe and
+        // the kernel addresses them relative to the chunk's first byte
+        auto row_byte = [&](uint64_t r) {
+            const uint64_t g = std::min(r / G, d.n_groups - 1);
+            return h->h_off[g] + (r - g * G) * h->h_rb[g];
+        };
         const uint64_t last = first_row + n_rows;
-        uint64_t ga = first_row / G;
-        const uint64_t gend = (last - 1) / G + 1;
-        while (ga < gend) {
-            uint64_t gb = ga + 1;
-            while (gb < gend && h->h_off[gb + 1] - h->h_off[ga] <= kStageBytes) ++gb;
-            const uint64_t bytes = h->h_off[gb] - h->h_off[ga];
-            if (bytes > kStageBytes) return fail(IBP_EINVAL, "a group is larger than the staging buffer");
+        uint64_t r = first_row;
+        while (r < last) {
+            const uint64_t byte0 = row_byte(r);
+            // the furthest row end e <= last with row_byte(e) - byte0 <= kStageBytes
+            uint64_t lo = r, hi = last;
+            while (lo < hi) {
+                const uint64_t mid = lo + (hi - lo + 1) / 2;
+                if (row_byte(mid) - byte0 <= kStageBytes) lo = mid; else hi = mid - 1;
+            }
+            if (lo == r) return fail(IBP_EINVAL, "a packed row is larger than the staging buffer");
+            const uint64_t e = lo, bytes = row_byte(e) - byte0;
             const int b = h->next_stage;
             h->next_stage = (h->next_stage + 1) % kStages;
             st = claim_stage(h, b, false);
             if (st != IBP_OK) return st;
             if (bytes)
-                IBP_HIP(h, hipMemcpyAsync(h->d_stage[b], h->h_payload + h->h_off[ga], bytes, hipMemcpyHostToDevice,
+                IBP_HIP(h, hipMemcpyAsync(h->d_stage[b], h->h_payload + byte0, bytes, hipMemcpyHostToDevice,
                                           h->copy_stream));
             IBP_HIP(h, hipEventRecord(h->ev_copied[b], h->copy_stream));
             IBP_HIP(h, hipStreamWaitEvent(s, h->ev_copied[b], 0));
-            const uint64_t r0 = std::max(first_row, ga * G), r1 = std::min(last, gb * G);
-            IBP_HIP(h, dev::launch_decompress(h->ds, h->d_stage[b], h->h_off[ga],
-                                              static_cast<uint8_t *>(d_out) + (r0 - first_row) * L, r0, r1 - r0, s));
+            IBP_HIP(h, dev::launch_decompress(h->ds, h->d_stage[b], byte0,
+                                              static_cast<uint8_t *>(d_out) + (r - first_row) * L, r, e - r, s));
             IBP_HIP(h, hipEventRecord(h->ev_free[b], s));
             h->stage_used[b] = true;
             h->stats.h2d_bytes += bytes;
             h->stats.h2d_payload_bytes += bytes;
-            ga = gb;
+            r = e;
         }
     }
     h->stats.calls += 1;

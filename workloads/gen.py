@@ -4,7 +4,8 @@ Conventions (so any row range can be regenerated on its own):
   * numpy Generator(PCG64) seeded with SeedSequence(seed, spawn_key=(purpose, chunk));
   * rows are drawn in chunks of CHUNK_ROWS = 2**20 rows, chunk c covering rows
     [c * CHUNK_ROWS, (c + 1) * CHUNK_ROWS);
-  * purposes: 0 = row values, 1 = batch ids, 2 = outlier channels, 3 = table permutations.
+  * purposes: 0 = row values, 1 = batch ids, 2 = outlier channels, 3 = table permutations,
+    4 = fixed-bit patterns of the decompression microbenchmark.
 
 The workloads stand in for the paper's datasets, which are not available here:
 OGB-Products-like GNN features, Criteo-like DLRM embedding tables, an LLM KV cache
@@ -18,7 +19,7 @@ import os
 import numpy as np
 
 CHUNK_ROWS = 1 << 20
-P_VALUES, P_IDS, P_OUTLIERS, P_PERM = 0, 1, 2, 3
+P_VALUES, P_IDS, P_OUTLIERS, P_PERM, P_MICRO = 0, 1, 2, 3, 4
 
 
 def chunk_rng(seed, purpose, chunk):
@@ -235,3 +236,34 @@ def structured_rows(kind, n_rows, row_bytes, seed=0):
     if kind == "smallint":
         return rng.integers(0, 16, size=(n_rows, e), dtype=np.uint32).view(np.uint8).reshape(shape)
     raise KeyError(kind)
+
+
+# ---------------------------------------------------------------- microbenchmark inputs
+
+def micro_rows(n_rows, row_bytes, fixed_fraction, seed=0, threads=None):
+    """Tensors for the decompression-overhead microbenchmark (the paper's Sec. 6.1
+    microbenchmark with synthetic metadata): n_rows tensors of row_bytes bytes in which
+    a seeded set of round(fixed_fraction * 8 * row_bytes) bit positions holds the same
+    seeded value in every tensor and every other bit is uniformly random. The fixed
+    positions are drawn once for the whole set, so every cluster of rows shares them.
+    """
+    n_bits = 8 * row_bytes
+    k = int(round(fixed_fraction * n_bits))
+    rng = chunk_rng(seed, P_MICRO, row_bytes)
+    pos = rng.permutation(n_bits)[:k]
+    fixed = np.zeros(n_bits, np.uint8)
+    fixed[pos] = 1
+    value = fixed & rng.integers(0, 2, size=n_bits, dtype=np.uint8)
+    keep = np.packbits(fixed, bitorder="little")          # bit p of the row = bit p%8 of byte p/8
+    val = np.packbits(value, bitorder="little")
+    out = np.empty((n_rows, row_bytes), np.uint8)
+
+    def fill(c):
+        a, b = c * CHUNK_ROWS, min(n_rows, (c + 1) * CHUNK_ROWS)
+        r = chunk_rng(seed, P_MICRO, (row_bytes << 20) + 1 + c).integers(0, 256, size=(b - a, row_bytes), dtype=np.uint8)
+        out[a:b] = (r & ~keep) | val
+
+    n_chunks = (n_rows + CHUNK_ROWS - 1) // CHUNK_ROWS
+    with ThreadPoolExecutor(threads or min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(fill, range(n_chunks)))
+    return out
