@@ -1,8 +1,10 @@
 """TEST INFRASTRUCTURE ONLY: the CPU oracle of Invariant Bit Packing.
 
 A plain, slow, single-threaded implementation written from the paper (Sec. 4.1-4.3
-and Sec. 6.5), used to check the library. Only tests/, __graft_entry__.smoke() and
-bench.py's CPU-baseline leg may import it; the product package never does.
+and Sec. 6.5): the clustered scheme with T = cluster size, and the thresholded scheme
+with participation bits and raw fallback. It is used to check the library. Only
+tests/, __graft_entry__.smoke() and bench.py's CPU-baseline leg may import it; the
+product package never does.
 
 The arithmetic lives in ibp_oracle.c (bit-serial C); this module only marshals
 numpy arrays into it. `OracleLib(path)` wraps any build of that file, so tests can
@@ -58,6 +60,21 @@ class OracleLib:
         lib.ibpo_compress.restype = ctypes.c_int
         lib.ibpo_decode_rows.argtypes = [_u8p, u64, ctypes.POINTER(ctypes.c_int64), u64, _u8p]
         lib.ibpo_decode_rows.restype = ctypes.c_int
+        lib.ibpo_thr_masks.argtypes = [_u8p, u64, u32, u32, u32, u32, _u8p, _u8p]
+        lib.ibpo_thr_masks.restype = None
+        lib.ibpo_part_row_bytes.argtypes = [_u8p, _u8p, _u8p, u32, u32]
+        lib.ibpo_part_row_bytes.restype = u64
+        lib.ibpo_part_pack_row.argtypes = [_u8p, _u8p, _u8p, u32, u32, _u8p]
+        lib.ibpo_part_pack_row.restype = None
+        lib.ibpo_part_unpack_row.argtypes = [_u8p, u64, _u8p, _u8p, u32, u32, _u8p]
+        lib.ibpo_part_unpack_row.restype = None
+        lib.ibpo_part_stream_bytes.argtypes = [_u8p, u64, u32, u32, u32, u32, u32, u32]
+        lib.ibpo_part_stream_bytes.restype = u64
+        lib.ibpo_part_compress.argtypes = [_u8p, u64, u32, u32, u32, u32, u32, u32, _u8p, u64,
+                                           ctypes.POINTER(u64)]
+        lib.ibpo_part_compress.restype = ctypes.c_int
+        lib.ibpo_part_decode_rows.argtypes = [_u8p, u64, ctypes.POINTER(ctypes.c_int64), u64, _u8p]
+        lib.ibpo_part_decode_rows.restype = ctypes.c_int
         self.lib = lib
         self.path = path
 
@@ -95,8 +112,49 @@ class OracleLib:
         b, n, L = _as_rows(rows)
         return int(self.lib.ibpo_stream_bytes(_u8(b), n, L, group_rows))
 
-    def compress(self, rows, group_rows):
-        """The whole compressed stream (numpy uint8) of rows in clusters of group_rows."""
+    # ---- thresholded scheme with participation bits (Sec. 4.1-4.2, T < N)
+
+    def thr_masks(self, rows, num, den, every=1):
+        """Mask and Bitval of one cluster under T = (num/den) * n over every k-th row."""
+        b, n, L = _as_rows(rows)
+        m = np.zeros(L, np.uint8)
+        v = np.zeros(L, np.uint8)
+        self.lib.ibpo_thr_masks(_u8(b), n, L, num, den, every, _u8(m), _u8(v))
+        return m, v
+
+    def part_row_bytes(self, row, mask, bitval, chunk_bytes):
+        r = np.ascontiguousarray(row).view(np.uint8).reshape(-1)
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        v = np.ascontiguousarray(bitval, dtype=np.uint8)
+        return int(self.lib.ibpo_part_row_bytes(_u8(r), _u8(m), _u8(v), m.size, chunk_bytes))
+
+    def part_pack_row(self, row, mask, bitval, chunk_bytes):
+        r = np.ascontiguousarray(row).view(np.uint8).reshape(-1)
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        v = np.ascontiguousarray(bitval, dtype=np.uint8)
+        out = np.zeros(self.part_row_bytes(r, m, v, chunk_bytes), np.uint8)
+        self.lib.ibpo_part_pack_row(_u8(r), _u8(m), _u8(v), m.size, chunk_bytes, _u8(out))
+        return out
+
+    def part_unpack_row(self, packed, mask, bitval, chunk_bytes):
+        p = np.ascontiguousarray(packed, dtype=np.uint8)
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        v = np.ascontiguousarray(bitval, dtype=np.uint8)
+        out = np.zeros(m.size, np.uint8)
+        self.lib.ibpo_part_unpack_row(_u8(p), p.size, _u8(m), _u8(v), m.size, chunk_bytes, _u8(out))
+        return out
+
+    def compress(self, rows, group_rows, chunk_bytes=0, threshold=(1, 1), sample_every=1):
+        """The whole compressed stream (numpy uint8) of rows in clusters of group_rows.
+
+        chunk_bytes = 0: the clustered scheme with T = cluster size and no participation
+        bits (threshold must be (1, 1), every row counted). chunk_bytes > 0: the
+        thresholded scheme, T = threshold[0] / threshold[1] of the counted rows, one
+        participation bit per chunk, counters over every sample_every-th row."""
+        if chunk_bytes:
+            return self._part_compress(rows, group_rows, chunk_bytes, threshold, sample_every)
+        if tuple(threshold) != (1, 1) or sample_every != 1:
+            raise ValueError("a threshold below 1 or a sampled Mask needs participation bits (chunk_bytes > 0)")
         b, n, L = _as_rows(rows)
         size = self.lib.ibpo_stream_bytes(_u8(b), n, L, group_rows)
         if size == 0:
@@ -108,14 +166,28 @@ class OracleLib:
             raise RuntimeError(f"ibpo_compress failed with {rc}")
         return out
 
+    def _part_compress(self, rows, group_rows, chunk_bytes, threshold, sample_every):
+        b, n, L = _as_rows(rows)
+        num, den = threshold
+        size = self.lib.ibpo_part_stream_bytes(_u8(b), n, L, group_rows, chunk_bytes, num, den, sample_every)
+        if size == 0:
+            raise ValueError("bad arguments for the participation scheme")
+        out = np.zeros(size, np.uint8)
+        got = ctypes.c_uint64(0)
+        rc = self.lib.ibpo_part_compress(_u8(b), n, L, group_rows, chunk_bytes, num, den, sample_every,
+                                         _u8(out), size, ctypes.byref(got))
+        if rc != 0:
+            raise RuntimeError(f"ibpo_part_compress failed with {rc}")
+        return out
+
     def decode_rows(self, stream, ids, row_bytes):
         """Rows `ids` of a stream decoded bit by bit: uint8 array (n_ids, row_bytes)."""
         s = np.ascontiguousarray(stream, dtype=np.uint8)
         i = np.ascontiguousarray(ids, dtype=np.int64)
         out = np.zeros((i.size, row_bytes), np.uint8)
-        rc = self.lib.ibpo_decode_rows(_u8(s), s.size,
-                                       i.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
-                                       i.size, _u8(out))
+        part = s.size >= 64 and int(s[32:36].view(np.uint32)[0]) == 1
+        fn = self.lib.ibpo_part_decode_rows if part else self.lib.ibpo_decode_rows
+        rc = fn(_u8(s), s.size, i.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), i.size, _u8(out))
         if rc != 0:
             raise ValueError(f"ibpo_decode_rows failed with {rc}")
         return out
@@ -155,8 +227,24 @@ def stream_bytes(rows, group_rows):
     return default().stream_bytes(rows, group_rows)
 
 
-def compress(rows, group_rows):
-    return default().compress(rows, group_rows)
+def compress(rows, group_rows, chunk_bytes=0, threshold=(1, 1), sample_every=1):
+    return default().compress(rows, group_rows, chunk_bytes, threshold, sample_every)
+
+
+def thr_masks(rows, num, den, every=1):
+    return default().thr_masks(rows, num, den, every)
+
+
+def part_row_bytes(row, mask, bitval, chunk_bytes):
+    return default().part_row_bytes(row, mask, bitval, chunk_bytes)
+
+
+def part_pack_row(row, mask, bitval, chunk_bytes):
+    return default().part_pack_row(row, mask, bitval, chunk_bytes)
+
+
+def part_unpack_row(packed, mask, bitval, chunk_bytes):
+    return default().part_unpack_row(packed, mask, bitval, chunk_bytes)
 
 
 def decode_rows(stream, ids, row_bytes):

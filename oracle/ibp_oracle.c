@@ -32,8 +32,28 @@
  *     group Mask then Bitval, a u64 offset index, then the packed rows back to back
  *     with no padding between rows, as the paper keeps tensors byte-aligned).
  *
+ *
+ * The thresholded scheme with participation bits (the paper's primary form, Sec. 4.1
+ * and 4.2 with T < N), in the same container with header flag bit 0 set:
+ *   - ibpo_thr_masks: Sec. 4.1 with a threshold T = (num/den) * n over the counters
+ *     of the cluster's rows (or of every k-th row, a sampled Mask): counter >= T
+ *     gives Mask 1 / Bitval 1, else n - counter >= T gives Mask 1 / Bitval 0, else
+ *     Mask 0 / Bitval 0 (inclusive inequalities; 2 num > den so at most one holds).
+ *   - ibpo_part_row_bytes: Sec. 4.2 and Fig. 4 -- a chunk of CS bytes is compressible
+ *     when chunk AND Mask equals Bitval on all its bits; bits saved = the Mask bits of
+ *     the compressible chunks; with one participation bit per chunk the bytes saved
+ *     are floor((saved - chunks) / 8); a row that saves no byte is stored raw (L bytes,
+ *     no participation bits), any other row takes L - bytes saved.
+ *   - ibpo_part_pack_row: Sec. 4.2 -- the participation bits first (bit c set when
+ *     chunk c is compressed), then chunk by chunk the row's bits in ascending order,
+ *     skipping the Mask bits of compressed chunks; LSB-first, zero padding.
+ *   - ibpo_part_unpack_row: Sec. 4.3 -- the reverse walk; a raw row is copied.
+ *   - rows are addressed by a u64 offset per row (the paper keeps in-place slots and a
+ *     compressed/raw bitmask, Sec. 5; here a row's size both locates it and tells a
+ *     raw row, size L, from a compressed one, size < L).
+ *
  * Parity status: every function here is pinned by tests (brute force on tiny
- * inputs, closed forms, identities and a hand-derived worked example).
+ * inputs, closed forms, identities and hand-derived worked examples).
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -261,6 +281,218 @@ int ibpo_decode_rows(const uint8_t *stream, uint64_t stream_bytes,
         uint64_t rb = ibpo_packed_row_bytes(mask, L);
         uint64_t off = get_u64(stream + index_off + 8 * g);
         ibpo_unpack_row(stream + payload_off + off + r * rb, mask, bitval, L, out + i * L);
+    }
+    return 0;
+}
+
+
+/* ======================= thresholded scheme with participation bits ========== */
+
+#define IBPO_FLAG_PARTICIPATION 1u
+
+/* Sec. 4.1 with T = (num/den) * n, over rows 0, every, 2*every, ... of the cluster. */
+void ibpo_thr_masks(const uint8_t *rows, uint64_t n_rows, uint32_t L, uint32_t num,
+                    uint32_t den, uint32_t every, uint8_t *mask, uint8_t *bitval)
+{
+    uint64_t nbits = 8ull * L;
+    uint64_t *counter = (uint64_t *)calloc(nbits, sizeof(uint64_t));
+    uint64_t n = 0;
+    for (uint64_t i = 0; i < n_rows; i += every) {
+        for (uint64_t p = 0; p < nbits; ++p)
+            counter[p] += (uint64_t)get_bit(rows + i * L, p);
+        ++n;
+    }
+    memset(mask, 0, L);
+    memset(bitval, 0, L);
+    for (uint64_t p = 0; p < nbits; ++p) {
+        /* counter >= T  <=>  counter * den >= num * n (exact in integers) */
+        if (counter[p] * den >= (uint64_t)num * n) {
+            set_bit(mask, p, 1);
+            set_bit(bitval, p, 1);
+        } else if ((n - counter[p]) * den >= (uint64_t)num * n) {
+            set_bit(mask, p, 1);
+        }
+    }
+    free(counter);
+}
+
+/* Is chunk c (CS bytes) of the row compressible: row AND Mask == Bitval on it? */
+static int chunk_matches(const uint8_t *row, const uint8_t *mask, const uint8_t *bitval,
+                         uint32_t CS, uint64_t c)
+{
+    for (uint64_t p = 8ull * CS * c; p < 8ull * CS * (c + 1); ++p)
+        if (get_bit(mask, p) && get_bit(row, p) != get_bit(bitval, p))
+            return 0;
+    return 1;
+}
+
+/* Bytes of one row in the participation scheme (L when stored raw). */
+uint64_t ibpo_part_row_bytes(const uint8_t *row, const uint8_t *mask, const uint8_t *bitval,
+                             uint32_t L, uint32_t CS)
+{
+    uint64_t chunks = L / CS;
+    uint64_t saved = 0;
+    for (uint64_t c = 0; c < chunks; ++c) {
+        if (!chunk_matches(row, mask, bitval, CS, c))
+            continue;
+        for (uint64_t p = 8ull * CS * c; p < 8ull * CS * (c + 1); ++p)
+            saved += (uint64_t)get_bit(mask, p);
+    }
+    if (saved < chunks + 8)       /* bytes saved = floor((saved - chunks) / 8) <= 0 */
+        return L;
+    return (uint64_t)L - (saved - chunks) / 8;
+}
+
+void ibpo_part_pack_row(const uint8_t *row, const uint8_t *mask, const uint8_t *bitval,
+                        uint32_t L, uint32_t CS, uint8_t *out)
+{
+    uint64_t size = ibpo_part_row_bytes(row, mask, bitval, L, CS);
+    if (size == L) {
+        memcpy(out, row, L);
+        return;
+    }
+    uint64_t chunks = L / CS;
+    memset(out, 0, size);
+    uint64_t k = 0;
+    for (uint64_t c = 0; c < chunks; ++c)
+        set_bit(out, k++, chunk_matches(row, mask, bitval, CS, c));
+    for (uint64_t c = 0; c < chunks; ++c) {
+        int comp = chunk_matches(row, mask, bitval, CS, c);
+        for (uint64_t p = 8ull * CS * c; p < 8ull * CS * (c + 1); ++p) {
+            if (comp && get_bit(mask, p))
+                continue;
+            set_bit(out, k++, get_bit(row, p));
+        }
+    }
+}
+
+void ibpo_part_unpack_row(const uint8_t *packed, uint64_t size, const uint8_t *mask,
+                          const uint8_t *bitval, uint32_t L, uint32_t CS, uint8_t *row)
+{
+    if (size == L) {
+        memcpy(row, packed, L);
+        return;
+    }
+    uint64_t chunks = L / CS;
+    memset(row, 0, L);
+    uint64_t k = chunks;
+    for (uint64_t c = 0; c < chunks; ++c) {
+        int comp = get_bit(packed, c);
+        for (uint64_t p = 8ull * CS * c; p < 8ull * CS * (c + 1); ++p) {
+            if (comp && get_bit(mask, p))
+                set_bit(row, p, get_bit(bitval, p));
+            else
+                set_bit(row, p, get_bit(packed, k++));
+        }
+    }
+}
+
+static int part_args_ok(uint32_t L, uint32_t G, uint32_t CS, uint32_t num, uint32_t den,
+                        uint32_t every)
+{
+    return L != 0 && L % 4 == 0 && G != 0 && CS != 0 && CS % 4 == 0 && L % CS == 0 &&
+           den != 0 && num <= den && 2ull * num > den && every != 0;
+}
+
+/* Stream bytes of the participation scheme; 0 on bad arguments. */
+uint64_t ibpo_part_stream_bytes(const uint8_t *rows, uint64_t n_rows, uint32_t L, uint32_t G,
+                                uint32_t CS, uint32_t num, uint32_t den, uint32_t every)
+{
+    if (!part_args_ok(L, G, CS, num, den, every))
+        return 0;
+    uint64_t ng = n_groups_of(n_rows, G);
+    uint64_t total = IBPO_HEADER_BYTES + ng * 2ull * L + 8ull * (n_rows + 1);
+    uint8_t *mask = (uint8_t *)malloc(L);
+    uint8_t *bitval = (uint8_t *)malloc(L);
+    for (uint64_t g = 0; g < ng; ++g) {
+        uint64_t n = rows_in_group(g, n_rows, G);
+        const uint8_t *grows = rows + g * G * (uint64_t)L;
+        ibpo_thr_masks(grows, n, L, num, den, every, mask, bitval);
+        for (uint64_t r = 0; r < n; ++r)
+            total += ibpo_part_row_bytes(grows + r * L, mask, bitval, L, CS);
+    }
+    free(mask);
+    free(bitval);
+    return total;
+}
+
+/*
+ * Compress in the participation scheme: header flags = 1 and the chunk bytes in the
+ * header word at offset 36, per cluster Mask then Bitval, a u64 offset per row
+ * (n_rows + 1 entries), then the rows back to back. Returns 0, 1 (bad arguments)
+ * or 2 (cap too small).
+ */
+int ibpo_part_compress(const uint8_t *rows, uint64_t n_rows, uint32_t L, uint32_t G,
+                       uint32_t CS, uint32_t num, uint32_t den, uint32_t every,
+                       uint8_t *out, uint64_t cap, uint64_t *out_bytes)
+{
+    if (!part_args_ok(L, G, CS, num, den, every))
+        return 1;
+    uint64_t total = ibpo_part_stream_bytes(rows, n_rows, L, G, CS, num, den, every);
+    *out_bytes = total;
+    if (total > cap)
+        return 2;
+    uint64_t ng = n_groups_of(n_rows, G);
+    uint64_t meta_off = IBPO_HEADER_BYTES;
+    uint64_t index_off = meta_off + ng * 2ull * L;
+    uint64_t payload_off = index_off + 8ull * (n_rows + 1);
+
+    memset(out, 0, IBPO_HEADER_BYTES);
+    memcpy(out, "IBP1", 4);
+    put_u32(out + 4, 1);
+    put_u32(out + 8, L);
+    put_u32(out + 12, G);
+    put_u64(out + 16, n_rows);
+    put_u64(out + 24, ng);
+    put_u32(out + 32, IBPO_FLAG_PARTICIPATION);
+    put_u32(out + 36, CS);
+    put_u64(out + 40, meta_off);
+    put_u64(out + 48, index_off);
+    put_u64(out + 56, payload_off);
+
+    uint64_t off = 0;
+    for (uint64_t g = 0; g < ng; ++g) {
+        uint64_t n = rows_in_group(g, n_rows, G);
+        const uint8_t *grows = rows + g * G * (uint64_t)L;
+        uint8_t *mask = out + meta_off + g * 2ull * L;
+        uint8_t *bitval = mask + L;
+        ibpo_thr_masks(grows, n, L, num, den, every, mask, bitval);
+        for (uint64_t r = 0; r < n; ++r) {
+            put_u64(out + index_off + 8 * (g * (uint64_t)G + r), off);
+            ibpo_part_pack_row(grows + r * L, mask, bitval, L, CS, out + payload_off + off);
+            off += ibpo_part_row_bytes(grows + r * L, mask, bitval, L, CS);
+        }
+    }
+    put_u64(out + index_off + 8 * n_rows, off);
+    return 0;
+}
+
+/* Decode rows of a participation-scheme stream. Returns 0, 1 (malformed) or 2 (range). */
+int ibpo_part_decode_rows(const uint8_t *stream, uint64_t stream_bytes,
+                          const int64_t *ids, uint64_t n_ids, uint8_t *out)
+{
+    if (stream_bytes < IBPO_HEADER_BYTES || memcmp(stream, "IBP1", 4) != 0 ||
+        get_u32(stream + 4) != 1 || get_u32(stream + 32) != IBPO_FLAG_PARTICIPATION)
+        return 1;
+    uint32_t L = get_u32(stream + 8);
+    uint32_t G = get_u32(stream + 12);
+    uint64_t n_rows = get_u64(stream + 16);
+    uint32_t CS = get_u32(stream + 36);
+    uint64_t meta_off = get_u64(stream + 40);
+    uint64_t index_off = get_u64(stream + 48);
+    uint64_t payload_off = get_u64(stream + 56);
+    if (L == 0 || G == 0 || CS == 0 || L % CS != 0)
+        return 1;
+    for (uint64_t i = 0; i < n_ids; ++i) {
+        if (ids[i] < 0 || (uint64_t)ids[i] >= n_rows)
+            return 2;
+        uint64_t id = (uint64_t)ids[i];
+        uint64_t g = id / G;
+        const uint8_t *mask = stream + meta_off + g * 2ull * L;
+        const uint8_t *bitval = mask + L;
+        uint64_t o0 = get_u64(stream + index_off + 8 * id);
+        uint64_t o1 = get_u64(stream + index_off + 8 * (id + 1));
+        ibpo_part_unpack_row(stream + payload_off + o0, o1 - o0, mask, bitval, L, CS, out + i * L);
     }
     return 0;
 }

@@ -12,7 +12,13 @@ pins come from the paper's definitions and from mathematics, never from the GPU 
     a cluster with an all-zero Mask packs every row to exactly its raw bytes;
   * the bound the first synthetic workload must meet (sign bit, bit 30 and
     mantissa bits 15..0 are invariant in every cluster, so a row packs to <= 224 B).
+
+The thresholded scheme with participation bits is pinned the same way: hand-derived
+examples (tests/golden/participation_examples.txt), brute force with exact rational
+thresholds and whole-chunk integer comparisons, its reduction to the clustered scheme
+at T = n, sampling as counting over the sampled rows only, and a closed form.
 """
+from fractions import Fraction
 import os
 
 import numpy as np
@@ -20,6 +26,7 @@ import numpy as np
 from workloads import CONFIGS, gen_rows, structured_rows
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "worked_examples.txt")
+GOLDEN_PART = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "participation_examples.txt")
 HEADER = 64
 
 
@@ -248,6 +255,237 @@ def pin_tiny_gnn_bound(orc):
         assert orc.packed_row_bytes(m) <= 224, g
 
 
+# ------------------------------------------ thresholded scheme, participation bits
+
+def parse_golden_part(path=GOLDEN_PART):
+    examples, cur = [], None
+    for line in open(path):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        tok = line.split()
+        if tok[0] == "name":
+            cur = {"name": tok[1], "rows": [], "size": {}, "packed": {}}
+        elif tok[0] in ("L", "G", "chunk"):
+            cur[tok[0]] = int(tok[1])
+        elif tok[0] == "threshold":
+            cur["threshold"] = (int(tok[1]), int(tok[2]))
+        elif tok[0] == "row":
+            cur["rows"].append(bytes.fromhex(tok[1]))
+        elif tok[0] in ("mask", "bitval"):
+            cur[tok[0]] = bytes.fromhex(tok[1])
+        elif tok[0] == "size":
+            cur["size"][int(tok[1])] = int(tok[2])
+        elif tok[0] == "packed":
+            cur["packed"][int(tok[1])] = bytes.fromhex(tok[2])
+        elif tok[0] == "stream":
+            cur["stream"] = bytes.fromhex("".join(tok[1:]))
+        elif tok[0] == "end":
+            examples.append(cur)
+            cur = None
+    return examples
+
+
+def brute_thr_masks(rows, num, den, every=1):
+    """Mask/Bitval as exact fractions of the counted rows agreeing on each bit."""
+    counted = [bits_of(bytes(r)) for r in rows[::every]]
+    n, t = len(counted), Fraction(num, den)
+    nbits = len(counted[0])
+    mask, bitval = [0] * nbits, [0] * nbits
+    for p in range(nbits):
+        ones = Fraction(sum(b[p] for b in counted), n)
+        if ones >= t:
+            mask[p], bitval[p] = 1, 1
+        elif 1 - ones >= t:
+            mask[p] = 1
+    return _to_bytes(mask), _to_bytes(bitval)
+
+
+def brute_part_pack(row, mask, bitval, cs):
+    """The participation-scheme encoding of one row, chunk by chunk with whole-chunk
+    integer comparisons; returns the packed bytes (the raw row when nothing is saved)."""
+    row, mask, bitval = bytes(row), bytes(mask), bytes(bitval)
+    L = len(row)
+    chunks = L // cs
+    comp, saved = [], 0
+    for c in range(chunks):
+        x = int.from_bytes(row[c * cs:(c + 1) * cs], "little")
+        m = int.from_bytes(mask[c * cs:(c + 1) * cs], "little")
+        b = int.from_bytes(bitval[c * cs:(c + 1) * cs], "little")
+        ok = (x & m) == b
+        comp.append(ok)
+        saved += bin(m).count("1") if ok else 0
+    if saved - chunks < 8:
+        return row
+    out = [1 if ok else 0 for ok in comp]
+    for c in range(chunks):
+        x = int.from_bytes(row[c * cs:(c + 1) * cs], "little")
+        m = int.from_bytes(mask[c * cs:(c + 1) * cs], "little")
+        for q in range(8 * cs):
+            if comp[c] and (m >> q) & 1:
+                continue
+            out.append((x >> q) & 1)
+    size = L - (saved - chunks) // 8
+    packed = _to_bytes(out)
+    return packed + bytes(size - len(packed))
+
+
+def part_closed_form_bytes(rows, G, cs, num, den, every):
+    n, L = rows.shape
+    ng = (n + G - 1) // G
+    total = HEADER + ng * 2 * L + 8 * (n + 1)
+    for g in range(ng):
+        grp = rows[g * G:(g + 1) * G]
+        m, v = brute_thr_masks(grp, num, den, every) if L <= 16 else _np_thr_masks(grp, num, den, every)
+        for r in grp:
+            total += len(brute_part_pack(r, m, v, cs))
+    return total
+
+
+def _np_thr_masks(rows, num, den, every):
+    """numpy form of the threshold rule for wider rows (exact integer comparisons)."""
+    sel = rows[::every]
+    n = sel.shape[0]
+    cnt = np.unpackbits(sel, axis=1, bitorder="little").sum(axis=0).astype(np.int64)
+    one = cnt * den >= num * n
+    zero = ~one & ((n - cnt) * den >= num * n)
+    return (bytes(np.packbits(one | zero, bitorder="little")),
+            bytes(np.packbits(one, bitorder="little")))
+
+
+def pin_part_worked_examples(orc):
+    for ex in parse_golden_part():
+        L, G, cs, (num, den) = ex["L"], ex["G"], ex["chunk"], ex["threshold"]
+        rows = np.frombuffer(b"".join(ex["rows"]), np.uint8).reshape(-1, L)
+        m, v = orc.thr_masks(rows, num, den)
+        assert bytes(m) == ex["mask"] and bytes(v) == ex["bitval"], (ex["name"], "masks")
+        for r in range(rows.shape[0]):
+            assert orc.part_row_bytes(rows[r], m, v, cs) == ex["size"][r], (ex["name"], "size", r)
+            assert bytes(orc.part_pack_row(rows[r], m, v, cs)) == ex["packed"][r], (ex["name"], "packed", r)
+            got = orc.part_unpack_row(np.frombuffer(ex["packed"][r], np.uint8), m, v, cs)
+            assert bytes(got) == bytes(rows[r]), (ex["name"], "unpack", r)
+        s = orc.compress(rows, G, chunk_bytes=cs, threshold=(num, den))
+        assert bytes(s) == ex["stream"], (ex["name"], "stream")
+        assert np.array_equal(orc.decompress(s, rows.shape[0], L), rows), (ex["name"], "decode")
+
+
+def pin_part_bruteforce(orc, trials=80, seed=5):
+    """Random small clusters with structure, random thresholds, chunk sizes and sampling."""
+    rng = np.random.default_rng(seed)
+    for t in range(trials):
+        cs = int(rng.choice([4, 8]))
+        L = cs * int(rng.integers(1, 4))
+        n = int(rng.integers(1, 12))
+        base = rng.integers(0, 256, size=L, dtype=np.uint8)
+        rows = np.tile(base, (n, 1))
+        for i in range(n):
+            for _ in range(int(rng.integers(0, 10))):
+                p = int(rng.integers(0, 8 * L))
+                rows[i, p // 8] ^= np.uint8(1 << (p % 8))
+        den = int(rng.integers(2, 11))
+        num = int(rng.integers(den // 2 + 1, den + 1))
+        every = int(rng.choice([1, 1, 2, 3]))
+        m, v = orc.thr_masks(rows, num, den, every)
+        bm, bv = brute_thr_masks(rows, num, den, every)
+        assert bytes(m) == bm and bytes(v) == bv, ("thr masks", t)
+        for i in range(n):
+            want = brute_part_pack(rows[i], bm, bv, cs)
+            got = orc.part_pack_row(rows[i], m, v, cs)
+            assert orc.part_row_bytes(rows[i], m, v, cs) == len(want), ("size", t, i)
+            assert bytes(got) == want, ("pack", t, i)
+            assert bytes(orc.part_unpack_row(got, m, v, cs)) == bytes(rows[i]), ("unpack", t, i)
+
+
+def pin_part_random_metadata(orc, trials=200, seed=6):
+    """Any Mask/Bitval (Bitval inside Mask), not only ones derived from the rows: the
+    encoding and the raw fallback must still round-trip and match brute force."""
+    rng = np.random.default_rng(seed)
+    for t in range(trials):
+        cs = int(rng.choice([4, 8, 12]))
+        L = cs * int(rng.integers(1, 3))
+        row = rng.integers(0, 256, size=L, dtype=np.uint8)
+        mask = rng.integers(0, 256, size=L, dtype=np.uint8) | (0xFF if t % 3 == 0 else 0)
+        mask = mask.astype(np.uint8)
+        bitval = (rng.integers(0, 256, size=L, dtype=np.uint8) & mask).astype(np.uint8)
+        if t % 2 == 0:      # make most chunks match
+            bitval = (row & mask).astype(np.uint8)
+            j = int(rng.integers(0, L))
+            bitval[j] ^= mask[j] & np.uint8(1 << int(rng.integers(0, 8)))
+        want = brute_part_pack(row, mask, bitval, cs)
+        got = orc.part_pack_row(row, mask, bitval, cs)
+        assert bytes(got) == want, ("pack", t)
+        assert bytes(orc.part_unpack_row(got, mask, bitval, cs)) == bytes(row), ("unpack", t)
+
+
+def pin_part_raw_fallback_boundary(orc):
+    """A row of C chunks that saves `saved` Mask bits is stored raw exactly while
+    saved - C < 8 (bytes saved = floor((saved - C) / 8) <= 0): sweep saved across that
+    boundary with every chunk compressible, for several chunk counts."""
+    rng = np.random.default_rng(11)
+    for L, cs in [(32, 4), (64, 8), (16, 4), (48, 4)]:
+        chunks = L // cs
+        for saved in range(0, min(8 * L, chunks + 20)):
+            row = rng.integers(0, 256, size=L, dtype=np.uint8)
+            pos = rng.permutation(8 * L)[:saved]
+            mbits = np.zeros(8 * L, np.uint8)
+            mbits[pos] = 1
+            mask = np.packbits(mbits, bitorder="little")
+            bitval = (row & mask).astype(np.uint8)          # every chunk compressible
+            size = orc.part_row_bytes(row, mask, bitval, cs)
+            want = L if saved - chunks < 8 else L - (saved - chunks) // 8
+            assert size == want, (L, cs, saved, size, want)
+            got = orc.part_pack_row(row, mask, bitval, cs)
+            assert bytes(got) == brute_part_pack(row, mask, bitval, cs), (L, cs, saved)
+            assert bytes(orc.part_unpack_row(got, mask, bitval, cs)) == bytes(row), (L, cs, saved)
+
+
+def pin_part_reduces_to_clustered(orc):
+    """At T = n every counted row agrees on every Mask bit, so every chunk participates:
+    the masks equal the clustered scheme's, each row's part bits are all 1, and the bits
+    after them are the clustered scheme's packed bits."""
+    for kind, n, L, G, cs in [("floats", 64, 64, 32, 4), ("sparse", 40, 128, 16, 8), ("smallint", 33, 16, 32, 4),
+                              ("onebit", 20, 24, 10, 8)]:
+        rows = structured_rows(kind, n, L, seed=n * L)
+        for g in range((n + G - 1) // G):
+            grp = rows[g * G:(g + 1) * G]
+            m1, v1 = orc.group_masks(grp)
+            m2, v2 = orc.thr_masks(grp, 1, 1, 1)
+            assert bytes(m1) == bytes(m2) and bytes(v1) == bytes(v2), (kind, g)
+            chunks = L // cs
+            for r in grp:
+                pk = orc.part_pack_row(r, m2, v2, cs)
+                if pk.size == L and (8 * L - popcount_bytes(m1)) + chunks > 8 * L - 8:
+                    continue      # nothing saved: stored raw
+                bits = np.unpackbits(pk, bitorder="little")
+                assert bits[:chunks].all(), (kind, "part bits")
+                v1bits = np.unpackbits(orc.pack_row(r, m1), bitorder="little")[:8 * L - popcount_bytes(m1)]
+                assert np.array_equal(bits[chunks:chunks + v1bits.size], v1bits), (kind, "payload")
+
+
+def pin_part_sampling_and_closed_form(orc):
+    """Sampled masks count only rows 0, k, 2k, ... of each cluster; stream size by the
+    closed form 64 + n_groups * 2L + 8 (n + 1) + sum of row sizes; round trips."""
+    cases = [("floats", 70, 16, 32, 4, (4, 5), 1), ("sparse", 50, 32, 64, 8, (3, 4), 2),
+             ("random", 21, 8, 7, 4, (9, 10), 1), ("specials", 40, 16, 40, 8, (7, 10), 3),
+             ("smallint", 33, 12, 11, 4, (1, 1), 1), ("floats", 1, 8, 4, 8, (4, 5), 1)]
+    for kind, n, L, G, cs, (num, den), every in cases:
+        rows = structured_rows(kind, n, L, seed=n + 7 * L)
+        for g in range((n + G - 1) // G):
+            grp = rows[g * G:(g + 1) * G]
+            m, v = orc.thr_masks(grp, num, den, every)
+            ms, vs = orc.thr_masks(np.ascontiguousarray(grp[::every]), num, den, 1)
+            assert bytes(m) == bytes(ms) and bytes(v) == bytes(vs), ("sampling", kind, g)
+        s = orc.compress(rows, G, chunk_bytes=cs, threshold=(num, den), sample_every=every)
+        assert s.size == part_closed_form_bytes(rows, G, cs, num, den, every), ("closed form", kind)
+        assert int(s[32:36].view(np.uint32)[0]) == 1 and int(s[36:40].view(np.uint32)[0]) == cs
+        assert np.array_equal(orc.decompress(s, n, L), rows), ("round trip", kind)
+        ids = np.random.default_rng(n).integers(0, n, size=2 * n)
+        assert np.array_equal(orc.decode_rows(s, ids, L), rows[ids]), ("gather", kind)
+
+
 ALL_PINS = [pin_worked_examples, pin_bruteforce_random, pin_exhaustive_alphabet,
             pin_zero_mask_is_identity, pin_identical_and_single_rows,
-            pin_closed_form_and_round_trip, pin_tiny_gnn_bound]
+            pin_closed_form_and_round_trip, pin_tiny_gnn_bound,
+            pin_part_worked_examples, pin_part_bruteforce, pin_part_random_metadata,
+            pin_part_raw_fallback_boundary, pin_part_reduces_to_clustered,
+            pin_part_sampling_and_closed_form]

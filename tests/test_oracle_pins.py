@@ -46,6 +46,20 @@ MUTANTS = [
                                                   "        uint8_t *mask = bitval + L;")]),
     ("rows of a cluster packed with the wrong stride", [("out + payload_off + off + r * rb);",
                                                          "out + payload_off + off + r * L);")]),
+    # the thresholded scheme with participation bits
+    ("strict threshold inequality", [("if (counter[p] * den >= (uint64_t)num * n) {",
+                                      "if (counter[p] * den > (uint64_t)num * n) {")]),
+    ("sampled Mask counts every row", [("for (uint64_t i = 0; i < n_rows; i += every) {",
+                                        "for (uint64_t i = 0; i < n_rows; ++i) {")]),
+    ("raw fallback forgets the participation bits", [("if (saved < chunks + 8)", "if (saved < 8)")]),
+    ("Mask bits dropped from raw chunks too", [("if (comp && get_bit(mask, p))\n                continue;",
+                                                "if (get_bit(mask, p))\n                continue;")]),
+    ("participation bit polarity flipped on both sides",
+     [("set_bit(out, k++, chunk_matches(row, mask, bitval, CS, c));",
+       "set_bit(out, k++, !chunk_matches(row, mask, bitval, CS, c));"),
+      ("int comp = get_bit(packed, c);", "int comp = !get_bit(packed, c);")]),
+    ("row offset index shifted by one row", [("put_u64(out + index_off + 8 * (g * (uint64_t)G + r), off);",
+                                              "put_u64(out + index_off + 8 * (g * (uint64_t)G + r + 1), off);")]),
 ]
 
 
