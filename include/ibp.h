@@ -25,9 +25,11 @@
  *
  * Compressed stream layout (version 1, little-endian, no implicit padding):
  *   [0,64)   header: "IBP1", u32 version=1, u32 row_bytes, u32 group_rows,
- *            u64 n_rows, u64 n_groups=ceil(n_rows/group_rows), u32 flags=0,
- *            u32 reserved=0, u64 meta_off=64, u64 index_off, u64 payload_off
+ *            u64 n_rows, u64 n_groups=ceil(n_rows/group_rows), u32 flags,
+ *            u32 chunk_bytes, u64 meta_off=64, u64 index_off, u64 payload_off
  *   meta     per group g: Mask_g[row_bytes] then Bitval_g[row_bytes]
+ *
+ * flags = 0, chunk_bytes = 0 -- the clustered scheme (T = cluster size):
  *   index    u64 off[0..n_groups], off[0]=0, off[g+1]=off[g]+n_g*rb_g where
  *            rb_g = row_bytes - floor(popcount(Mask_g)/8) (Fig. 4 size rule with no
  *            participation bits: under T = cluster size every chunk matches Bitval)
@@ -35,6 +37,19 @@
  *            payload_off + off[g] + r*rb_g; packed bit k is bit k%8 of byte k/8 and
  *            holds the k-th variant bit of the row in ascending bit position
  *            (row bit p = bit p%8 of byte p/8); padding bits are zero.
+ *
+ * flags = 1 (IBP_STREAM_PARTICIPATION) -- the thresholded scheme of Sec. 4.1-4.2:
+ *   Mask/Bitval from a threshold T < n (rows may disagree with Bitval), the row cut
+ *   into chunks of chunk_bytes (a multiple of 4 dividing row_bytes), one
+ *   participation bit per chunk:
+ *   index    u64 off[0..n_rows], off[0]=0: row i occupies [off[i], off[i+1]) of the
+ *            payload (rows back to back)
+ *   payload  a row of size row_bytes is stored raw (no byte would be saved); any other
+ *            row is: bit c (c < C = row_bytes/chunk_bytes) = 1 when chunk c is
+ *            compressed (chunk AND Mask == Bitval), then chunk by chunk the row's
+ *            bits in ascending position, leaving out the Mask bits of compressed
+ *            chunks; size = row_bytes - floor((S - C)/8) where S is the number of
+ *            Mask bits of its compressed chunks (S - C >= 8 for such a row).
  */
 #ifndef IBP_H
 #define IBP_H
@@ -67,7 +82,24 @@ typedef struct {
     uint64_t stream_bytes;   /* payload_off + payload_bytes */
     uint32_t row_bytes;
     uint32_t group_rows;
+    uint32_t flags;          /* 0 or IBP_STREAM_PARTICIPATION */
+    uint32_t chunk_bytes;    /* participation chunk bytes (0 for the clustered scheme) */
 } ibp_desc;
+
+/* Stream flags. */
+enum { IBP_STREAM_PARTICIPATION = 1 };
+
+/* Compression parameters of ibp_compress_ex. */
+typedef struct {
+    uint32_t group_rows;     /* rows per cluster (>= n_rows: one Mask for all rows) */
+    uint32_t chunk_bytes;    /* 0: the clustered scheme, no participation bits (then
+                                threshold_num must equal threshold_den and
+                                sample_every be 1); else the participation chunk size,
+                                a multiple of 4 dividing row_bytes */
+    uint32_t threshold_num;  /* T = threshold_num / threshold_den of the counted rows; */
+    uint32_t threshold_den;  /*   require threshold_den/2 < threshold_num <= threshold_den */
+    uint32_t sample_every;   /* count rows 0, k, 2k, ... of each cluster (1 = all rows) */
+} ibp_params;
 
 typedef struct {
     uint64_t calls;          /* decompress / gather calls that enqueued work */
@@ -117,10 +149,28 @@ ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes,
                         uint64_t *out_bytes);
 
 /*
+ * ibp_compress_ex -- compress with explicit parameters: the clustered scheme above
+ * (chunk_bytes = 0, same stream as ibp_compress) or the thresholded scheme with
+ * participation bits (Sec. 4.1-4.2): per cluster, bit p is invariant 1 when at least
+ * T of the counted rows have it set and invariant 0 when at least T have it clear
+ * (T = threshold_num/threshold_den of the counted rows, inclusive), then every row is
+ * encoded chunk by chunk as in the flags = 1 layout, or stored raw when it would save
+ * no byte. Host only, synchronous, re-entrant; n_threads <= 0 uses every online CPU.
+ * Call with out_cap = 0 to learn the size (*out_bytes, IBP_ENOMEM). The stream is a
+ * pure function of (rows, n_rows, row_bytes, *params).
+ * Errors: IBP_EINVAL (null pointers with n_rows > 0, bad row_bytes or parameters),
+ * IBP_ENOMEM (out_cap too small or a host allocation failed).
+ */
+ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes,
+                           const ibp_params *params, int n_threads, void *out,
+                           uint64_t out_cap, uint64_t *out_bytes);
+
+/*
  * ibp_describe -- validate a stream and fill *d. Host only. Validation covers the
  * header fields, the section offsets, Bitval being zero wherever Mask is zero, a
- * monotone index with off[0] = 0 and off[g+1] - off[g] = n_g * rb_g, and the stream
- * being at least payload_off + off[n_groups] bytes long.
+ * monotone index with off[0] = 0 and off[g+1] - off[g] = n_g * rb_g (clustered
+ * scheme) or every row's size agreeing with its participation bits (flags = 1), and
+ * the stream being at least payload_off + the last index entry bytes long.
  * Errors: IBP_EINVAL (null pointers), IBP_ECORRUPT (any validation failure).
  */
 ibp_status ibp_describe(const void *stream, uint64_t stream_bytes, ibp_desc *d);

@@ -23,6 +23,7 @@ STATUS_NAMES = {0: "IBP_OK", 1: "IBP_EINVAL", 2: "IBP_ERANGE", 3: "IBP_ENOMEM", 
 IBP_OPEN_PAYLOAD_DEVICE = 0
 IBP_OPEN_PAYLOAD_HOST = 1
 IBP_OPEN_PAYLOAD_HOST_ZERO_COPY = 2
+IBP_STREAM_PARTICIPATION = 1
 
 
 class IbpError(RuntimeError):
@@ -36,10 +37,17 @@ class ibp_desc(ctypes.Structure):
                 ("meta_off", ctypes.c_uint64), ("index_off", ctypes.c_uint64),
                 ("payload_off", ctypes.c_uint64), ("payload_bytes", ctypes.c_uint64),
                 ("stream_bytes", ctypes.c_uint64), ("row_bytes", ctypes.c_uint32),
-                ("group_rows", ctypes.c_uint32)]
+                ("group_rows", ctypes.c_uint32), ("flags", ctypes.c_uint32),
+                ("chunk_bytes", ctypes.c_uint32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class ibp_params(ctypes.Structure):
+    _fields_ = [("group_rows", ctypes.c_uint32), ("chunk_bytes", ctypes.c_uint32),
+                ("threshold_num", ctypes.c_uint32), ("threshold_den", ctypes.c_uint32),
+                ("sample_every", ctypes.c_uint32)]
 
 
 class ibp_stats(ctypes.Structure):
@@ -56,6 +64,7 @@ _vp, _u64, _u32, _i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctype
 _SIGS = {
     "ibp_compress_bound": [_u64, _u32, _u32, ctypes.POINTER(_u64)],
     "ibp_compress": [_vp, _u64, _u32, _u32, _i32, _vp, _u64, ctypes.POINTER(_u64)],
+    "ibp_compress_ex": [_vp, _u64, _u32, ctypes.POINTER(ibp_params), _i32, _vp, _u64, ctypes.POINTER(_u64)],
     "ibp_describe": [_vp, _u64, ctypes.POINTER(ibp_desc)],
     "ibp_open": [_vp, _u64, _i32, _u32, ctypes.POINTER(_vp)],
     "ibp_decompress": [_vp, _u64, _u64, _vp, _u64, _vp],
@@ -159,6 +168,26 @@ def ibp_compress_bound(n_rows, row_bytes, group_rows):
     out = _u64(0)
     _check(lib().ibp_compress_bound(n_rows, row_bytes, group_rows, ctypes.byref(out)), "ibp_compress_bound")
     return out.value
+
+
+def ibp_compress_ex(rows, group_rows, chunk_bytes=0, threshold=(1, 1), sample_every=1, n_threads=0):
+    """Compress with explicit parameters (include/ibp.h ibp_compress_ex): chunk_bytes = 0
+    is the clustered scheme; chunk_bytes > 0 the thresholded scheme with participation
+    bits, T = threshold[0] / threshold[1] of the counted rows (every sample_every-th)."""
+    a = np.ascontiguousarray(rows)
+    if a.ndim != 2:
+        raise ValueError("rows must be a 2-D array (n_rows, elements)")
+    n_rows, row_bytes = a.shape[0], a.shape[1] * a.itemsize
+    p = ibp_params(group_rows, chunk_bytes, threshold[0], threshold[1], sample_every)
+    got = _u64(0)
+    L = lib()
+    st = L.ibp_compress_ex(a.ctypes.data, n_rows, row_bytes, ctypes.byref(p), n_threads, None, 0, ctypes.byref(got))
+    if st != IBP_ENOMEM or got.value == 0:
+        _check(st, "ibp_compress_ex")
+    out = np.empty(got.value, np.uint8)
+    _check(L.ibp_compress_ex(a.ctypes.data, n_rows, row_bytes, ctypes.byref(p), n_threads, out.ctypes.data,
+                             got.value, ctypes.byref(got)), "ibp_compress_ex")
+    return out[:got.value]
 
 
 def ibp_compress(rows, group_rows, n_threads=0):

@@ -11,27 +11,31 @@ namespace dev {
 // What the kernels need to know about a stream resident on the device.
 struct DevStream {
     const uint32_t *meta;    // per group: Mask[W] then Bitval[W] (32-bit words)
-    const uint64_t *index;   // off[0..n_groups] (payload byte offsets)
+    const uint64_t *index;   // clustered scheme: off[0..n_groups] (payload byte offset of
+                             // each group); participation scheme: off[0..n_rows] (of each row)
     uint64_t n_rows;
     uint64_t n_groups;
     uint64_t g_magic;        // ceil(2^64 / G) for G >= 2: id / G = mulhi(id, g_magic)
     uint32_t W;              // 32-bit words per row
     uint32_t G;              // rows per group
+    uint32_t part_m;         // participation scheme: words per chunk; 0 = clustered scheme
 };
 
 uint64_t div_magic(uint32_t G);
 
 // Rows [first, first + n) into out (row-major). Packed row r of group g is read at byte
-// off[g] - pay_base + (r - g*G) * rb_g of `payload`, which must be readable for 8 bytes
-// past the last packed byte.
+// off[g] - pay_base + (r - g*G) * rb_g of `payload` (participation scheme: at byte
+// off[r] - pay_base, off[r+1] - off[r] bytes), which must be readable for 8 bytes past
+// the last packed byte.
 hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_t pay_base,
                              void *out, uint64_t first, uint64_t n, hipStream_t stream);
 
 // out[i] = row i of n requests. Device payload (sg == soff == null): request i is row
-// ids[i], read at off[g] + r*rb_g of the device-resident payload; ids outside
-// [0, n_rows) give a zero row and one increment of *err. Host-packed staging (ids null):
-// request i belongs to cluster sg[i] (validated on the host) and its packed bytes start
-// at byte soff[i] of `payload`. Either payload is readable 8 bytes past its last byte.
+// ids[i], read at off[g] + r*rb_g (participation scheme: off[id]) of the device-resident
+// payload; ids outside [0, n_rows) give a zero row and one increment of *err.
+// Host-packed staging (ids null): request i belongs to cluster sg[i] (validated on the
+// host) and its packed bytes are [soff[i], soff[i+1]) of `payload` (soff has n + 1
+// entries). Either payload is readable 8 bytes past its last byte.
 hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids,
                          const uint32_t *sg, const uint32_t *soff, uint64_t n, void *out,
                          unsigned long long *err, hipStream_t stream);

@@ -22,6 +22,8 @@
 //   * packed rows are byte-aligned and of any length, so a word's window is read as
 //     two dwords at its bit offset and funnel-shifted (v_alignbit_b32), never with
 //     sub-dword loads. No MFMA anywhere: nothing here is a contraction.
+#include <algorithm>
+
 #include "ibp_device.hpp"
 
 namespace ibp {
@@ -596,6 +598,171 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
     }
 }
 
+// ---- the thresholded scheme with participation bits (stream flags = 1) ----------
+//
+// A row is either raw (row_bytes long) or: C participation bits, then chunk by chunk
+// the row's bits, without the Mask bits of the compressed chunks. Which chunks are
+// compressed differs from row to row, so the word offsets are a scan per row: word w's
+// width is popcount(~Mask_w) when its chunk is compressed and 32 otherwise. The
+// cluster's tile (Mask/Bitval, precomputed runs) is set up once and kept while
+// consecutive rows share the cluster (with one global Mask, once per wave).
+
+enum { kSrcRange = 0, kSrcIds = 1, kSrcStaged = 2 };
+
+// Decode one tile (words [w0, w0 + 64K)) of one participation-scheme row whose bytes
+// start at byte `rbyte` of pay32; `start` is the bit of the row where this tile's first
+// word begins. Returns the tile's bits.
+template <int NR, int K, int MAXR>
+__device__ __forceinline__ uint32_t part_tile(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                              uint64_t rbyte, bool raw, uint32_t m, uint32_t start,
+                                              uint32_t W, uint32_t w0, uint32_t *__restrict__ orow) {
+    const uint32_t l = lane_id();
+    const uint32_t *__restrict__ p = pay32 + (rbyte >> 2);
+    const uint32_t bit0 = ((uint32_t)rbyte & 3u) * 8u;
+    // the participation bits of this tile's chunks: dwords dbase .. dbase + nd - 1 of
+    // the row's bit string, dword q in lane q - dbase
+    const uint32_t w_end = min(W, w0 + (uint32_t)(kWave * K));
+    const uint32_t dbase = (w0 / m) >> 5;
+    const uint32_t nd = (((w_end - 1) / m) >> 5) - dbase + 1;
+    uint32_t pd = 0;
+    if (!raw && l < nd) {
+        const uint32_t q = dbase + l;
+        pd = __builtin_amdgcn_alignbit(p[q + 1], p[q], bit0);
+    }
+    uint32_t width[K], pb[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const uint32_t w = w0 + l + kWave * j;
+        const uint32_t c = (w < W ? w : w0) / m;
+        const uint32_t dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)((((c >> 5) - dbase) & 63u) * 4u), (int)pd);
+        pb[j] = raw ? 0u : (dw >> (c & 31u)) & 1u;
+        width[j] = w < W ? (pb[j] ? (uint32_t)__builtin_popcount(t.nm[j]) : 32u) : 0u;
+    }
+    uint32_t ofs[K];
+    uint32_t c = 0;
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const uint32_t inc = wave_incl_scan(width[j]);
+        ofs[j] = c + inc - width[j];
+        c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+    }
+    uint32_t d0[K], d1[K], b[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        b[j] = bit0 + start + ofs[j];
+        d0[j] = p[b[j] >> 5];
+        d1[j] = p[(b[j] >> 5) + 1];
+    }
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const uint32_t x = __builtin_amdgcn_alignbit(d1[j], d0[j], b[j]);
+        uint32_t v;
+        if constexpr (NR >= 0) v = word_fast<NR>(t, j, x);
+        else v = word_generic(t.bv[j], t.nm[j], x);
+        v = pb[j] ? v : x;
+        const uint32_t w = w0 + l + kWave * j;
+        if (w < W) orow[w] = v;
+    }
+    return c;
+}
+
+template <int K, int MAXR>
+__device__ __forceinline__ uint32_t part_tile_any(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                                  uint64_t rbyte, bool raw, uint32_t m, uint32_t start,
+                                                  uint32_t W, uint32_t w0, uint32_t *__restrict__ orow) {
+    switch (t.nr) {   // wave-uniform
+    case 0: return part_tile<0>(t, pay32, rbyte, raw, m, start, W, w0, orow);
+    case 1: return part_tile<1>(t, pay32, rbyte, raw, m, start, W, w0, orow);
+    case 2: if constexpr (MAXR >= 2) return part_tile<2>(t, pay32, rbyte, raw, m, start, W, w0, orow); break;
+    case 3: if constexpr (MAXR >= 3) return part_tile<3>(t, pay32, rbyte, raw, m, start, W, w0, orow); break;
+    case 4: if constexpr (MAXR >= 4) return part_tile<4>(t, pay32, rbyte, raw, m, start, W, w0, orow); break;
+    default: break;
+    }
+    return part_tile<-1>(t, pay32, rbyte, raw, m, start, W, w0, orow);
+}
+
+// One wave decodes `per_wave` consecutive work items (rows of a range, requests of a
+// gather), one row at a time.
+template <int K, int MAXR, int SRC>
+__global__ __launch_bounds__(kBlock) void k_part_rows(DevStream s, const uint32_t *__restrict__ pay32,
+                                                       uint64_t pay_base, const int64_t *__restrict__ ids,
+                                                       const uint32_t *__restrict__ sg,
+                                                       const uint32_t *__restrict__ soff, uint64_t first,
+                                                       uint64_t n, uint32_t *__restrict__ out, uint32_t per_wave,
+                                                       unsigned long long *err) {
+    const uint64_t i0 = wave_slot() * per_wave;
+    if (i0 >= n) return;
+    const uint32_t cnt = (uint32_t)min((uint64_t)per_wave, n - i0);
+    const uint32_t l = lane_id();
+    const uint32_t W = s.W, m = s.part_m, C = W / m;
+    const bool one_tile = W <= (uint32_t)(kWave * K);
+    uint64_t cached_g = ~0ull;
+    Tile<K, MAXR> t;
+    for (uint32_t k = 0; k < cnt; ++k) {
+        const uint64_t i = i0 + k;
+        uint32_t *__restrict__ orow = out + i * W;
+        uint64_t g, rbyte, size;
+        if constexpr (SRC == kSrcStaged) {
+            g = sg[i];
+            rbyte = soff[i];
+            size = soff[i + 1] - soff[i];
+        } else {
+            uint64_t r;
+            if constexpr (SRC == kSrcIds) {
+                const int64_t id = ids[i];
+                if (id < 0 || (uint64_t)id >= s.n_rows) {
+                    for (uint32_t w = l; w < W; w += kWave) orow[w] = 0u;
+                    if (l == 0) atomicAdd(err, 1ull);
+                    continue;
+                }
+                r = (uint64_t)id;
+            } else {
+                r = first + i;
+            }
+            g = s.G == 1 ? r : __umul64hi(r, s.g_magic);
+            const uint64_t o0 = s.index[r];
+            rbyte = o0 - pay_base;
+            size = s.index[r + 1] - o0;
+        }
+        const bool raw = size == 4ull * W;
+        const uint32_t *__restrict__ mg = s.meta + g * 2ull * W;
+        if (one_tile) {
+            if (g != cached_g) {
+                tile_setup(t, mg, W, 0, 0);
+                cached_g = g;
+            }
+            part_tile_any(t, pay32, rbyte, raw, m, raw ? 0u : C, W, 0, orow);
+        } else {
+            uint32_t start = raw ? 0u : C;
+            for (uint32_t w0 = 0; w0 < W; w0 += kWave * K) {
+                tile_setup(t, mg, W, w0, 0);
+                start += part_tile_any(t, pay32, rbyte, raw, m, start, W, w0, orow);
+            }
+            cached_g = ~0ull;
+        }
+    }
+}
+
+template <int K, int MAXR>
+hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_base, const int64_t *ids,
+                         const uint32_t *sg, const uint32_t *soff, uint64_t first, uint64_t n, uint32_t *o,
+                         unsigned long long *err, hipStream_t stream) {
+    // about 16k waves when there is enough work, at most 16 rows per wave
+    const uint32_t per_wave = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(16, n / 16384));
+    const uint64_t waves = (n + per_wave - 1) / per_wave;
+    const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
+    if (ids)
+        hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcIds>), grid, block, 0, stream, s, p, pay_base, ids, sg, soff,
+                           first, n, o, per_wave, err);
+    else if (sg)
+        hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcStaged>), grid, block, 0, stream, s, p, pay_base, ids, sg,
+                           soff, first, n, o, per_wave, err);
+    else
+        hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcRange>), grid, block, 0, stream, s, p, pay_base, ids, sg,
+                           soff, first, n, o, per_wave, err);
+    return hipGetLastError();
+}
+
 // Words-per-lane tile shape for a row of W words: (K, MAXR).
 int pick_k(uint32_t W) {
     if (W <= 64) return 1;
@@ -614,9 +781,23 @@ uint64_t div_magic(uint32_t G) {
     return ~0ull / G + 1;
 }
 
+hipError_t launch_part(const DevStream &s, const uint8_t *payload, uint64_t pay_base, const int64_t *ids,
+                       const uint32_t *sg, const uint32_t *soff, uint64_t first, uint64_t n, void *out,
+                       unsigned long long *err, hipStream_t stream) {
+    const auto *p = reinterpret_cast<const uint32_t *>(payload);
+    auto *o = static_cast<uint32_t *>(out);
+    switch (pick_k(s.W)) {
+    case 1: return launch_part_k<1, 4>(s, p, pay_base, ids, sg, soff, first, n, o, err, stream);
+    case 2: return launch_part_k<2, 4>(s, p, pay_base, ids, sg, soff, first, n, o, err, stream);
+    case 4: return launch_part_k<4, 2>(s, p, pay_base, ids, sg, soff, first, n, o, err, stream);
+    default: return launch_part_k<8, 1>(s, p, pay_base, ids, sg, soff, first, n, o, err, stream);
+    }
+}
+
 hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_t pay_base, void *out,
                              uint64_t first, uint64_t n, hipStream_t stream) {
     if (n == 0) return hipSuccess;
+    if (s.part_m) return launch_part(s, payload, pay_base, nullptr, nullptr, nullptr, first, n, out, nullptr, stream);
     const uint64_t g0 = first / s.G, g1 = (first + n - 1) / s.G;
     // rows per wave: a whole cluster (at most 64 rows), halved while the launch would have
     // fewer than ~16k waves (2 per wave slot of the chip), down to one batch of rows;
@@ -643,6 +824,7 @@ hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_
 hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64_t *ids, const uint32_t *sg,
                          const uint32_t *soff, uint64_t n, void *out, unsigned long long *err, hipStream_t stream) {
     if (n == 0) return hipSuccess;
+    if (s.part_m) return launch_part(s, payload, 0, ids, sg, soff, 0, n, out, err, stream);
     const auto *p = reinterpret_cast<const uint32_t *>(payload);
     auto *o = static_cast<uint32_t *>(out);
     const int k = pick_k(s.W);

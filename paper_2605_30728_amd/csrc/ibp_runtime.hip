@@ -3,7 +3,8 @@
 //
 // Data layout in device memory (per handle):
 //   d_meta    n_groups * 2 * row_bytes  Mask then Bitval per group, as in the stream
-//   d_index   (n_groups + 1) u64        payload byte offset of every group
+//   d_index   (n_groups + 1) u64        payload byte offset of every group (participation
+//                                       scheme: (n_rows + 1) u64, of every row)
 //   d_payload payload_bytes + slack     packed rows (IBP_OPEN_PAYLOAD_DEVICE only; with
 //                                       IBP_OPEN_PAYLOAD_HOST_ZERO_COPY the kernels read
 //                                       the pinned host copy through its device address)
@@ -85,9 +86,9 @@ struct ibp_handle {
     int next_ids = 0;
     // PCIe path
     uint8_t *h_payload = nullptr;
-    std::vector<uint64_t> h_off;
-    std::vector<uint32_t> h_rb;
-    uint32_t max_rb = 0;            // largest packed row of any cluster
+    std::vector<uint64_t> h_off;    // the stream's index: per group, or per row (participation)
+    std::vector<uint32_t> h_rb;     // clustered scheme: packed row bytes of every group
+    uint32_t max_rb = 0;            // largest packed row
     uint8_t *h_stage[kStages] = {};
     uint8_t *d_stage[kStages] = {};
     hipStream_t copy_stream = nullptr;
@@ -96,6 +97,7 @@ struct ibp_handle {
     bool stage_used[kStages] = {};
     int next_stage = 0;
     std::vector<uint32_t> req_g, req_rb;   // per-request cluster and packed size (host gathers)
+    std::vector<uint64_t> req_src;         // payload byte of every request's packed row
     std::vector<uint64_t> blk_off;         // packed bytes of every packing block (host gathers)
     std::vector<uint64_t> chunk_off;       // staged byte offset of every block of one chunk
     Pool *pool = nullptr;
@@ -202,12 +204,18 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
         std::memcpy(dst + lo, src + lo, hi - lo);
     });
     std::memset(dst + d.payload_bytes, 0, kSlack);
-    h->h_off.resize(d.n_groups + 1);
-    h->h_rb.resize(d.n_groups);
-    for (uint64_t g = 0; g <= d.n_groups; ++g) h->h_off[g] = v.off(g);
-    for (uint64_t g = 0; g < d.n_groups; ++g) {
-        h->h_rb[g] = (uint32_t)((h->h_off[g + 1] - h->h_off[g]) / v.rows_in_group(g));
-        h->max_rb = std::max(h->max_rb, h->h_rb[g]);
+    if (d.flags & IBP_STREAM_PARTICIPATION) {
+        h->h_off.resize(d.n_rows + 1);
+        for (uint64_t r = 0; r <= d.n_rows; ++r) h->h_off[r] = v.off(r);
+        h->max_rb = d.row_bytes;        // a raw row
+    } else {
+        h->h_off.resize(d.n_groups + 1);
+        h->h_rb.resize(d.n_groups);
+        for (uint64_t g = 0; g <= d.n_groups; ++g) h->h_off[g] = v.off(g);
+        for (uint64_t g = 0; g < d.n_groups; ++g) {
+            h->h_rb[g] = (uint32_t)((h->h_off[g + 1] - h->h_off[g]) / v.rows_in_group(g));
+            h->max_rb = std::max(h->max_rb, h->h_rb[g]);
+        }
     }
     if (h->flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) return IBP_OK;   // no staging: kernels read in place
     if (d.n_groups > 0xFFFFFFFFull) return fail(IBP_EINVAL, "too many clusters for the PCIe path");
@@ -238,7 +246,8 @@ ibp_status claim_stage(ibp_handle *h, int b, bool host_side_too) {
 // PCIe gather: the host packs the requested packed rows into pinned staging chunk by
 // chunk, rotating kStages buffers, so that packing chunk k+1 overlaps the DMA of chunk k
 // and the decode of chunk k-1. A chunk's staging is [cluster of each request (u32) |
-// staged byte offset of each request (u32) | the packed rows, byte-packed].
+// staged byte offset of each request and the end of the last (u32, nc + 1 entries) |
+// the packed rows, byte-packed].
 ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, uint8_t *d_out, hipStream_t s) {
     const uint64_t L = h->d.row_bytes, G = h->d.group_rows;
     const uint64_t magic = dev::div_magic((uint32_t)G);
@@ -255,10 +264,14 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
     const uint64_t nblk_all = (n + blk - 1) / blk;
     h->req_g.resize(n);
     h->req_rb.resize(n);
+    h->req_src.resize(n);
     h->blk_off.assign(nblk_all + 1, 0);
     uint32_t *rg = h->req_g.data(), *rrb = h->req_rb.data();
+    uint64_t *rsrc = h->req_src.data();
     uint64_t *bs = h->blk_off.data();
     const uint32_t *grb = h->h_rb.data();
+    const uint64_t *hoff = h->h_off.data();
+    const bool part = h->d.flags & IBP_STREAM_PARTICIPATION;
     h->pool->run(nblk_all, 1, [&](uint64_t lo, uint64_t hi) {
         for (uint64_t k = lo; k < hi; ++k) {
             uint64_t sum = 0;
@@ -266,8 +279,14 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
                 const uint64_t id = (uint64_t)ids[i];
                 const uint64_t g = G == 1 ? id : (uint64_t)(((unsigned __int128)id * magic) >> 64);
                 rg[i] = (uint32_t)g;
-                rrb[i] = grb[g];
-                sum += grb[g];
+                if (part) {
+                    rsrc[i] = hoff[id];
+                    rrb[i] = (uint32_t)(hoff[id + 1] - hoff[id]);
+                } else {
+                    rsrc[i] = hoff[g] + (id - g * G) * grb[g];
+                    rrb[i] = grb[g];
+                }
+                sum += rrb[i];
             }
             bs[k + 1] = sum;
         }
@@ -282,7 +301,8 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
         uint8_t *stg = h->h_stage[b];
         uint32_t *sg = reinterpret_cast<uint32_t *>(stg);
         uint32_t *soff = sg + nc;
-        uint8_t *pay = stg + 8 * nc;
+        const uint64_t tables = 8 * nc + 4;
+        uint8_t *pay = stg + tables;
         // staged offsets: an exclusive scan over this chunk's block sums, then every block
         // writes its tables and copies its rows (prefetching a few rows ahead, since each
         // row is a random read of ~rb bytes from host memory)
@@ -292,17 +312,14 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
         bo[0] = 0;
         for (uint64_t k = 0; k < nblk; ++k) bo[k + 1] = bo[k] + bs[k0 + k + 1];
         const uint64_t total_pay = bo[nblk];
+        soff[nc] = (uint32_t)total_pay;
         const uint8_t *src_base = h->h_payload;
-        const uint64_t *goff = h->h_off.data();
         h->pool->run(nblk, 1, [&](uint64_t lo, uint64_t hi) {
             constexpr uint64_t kAhead = 12;
             for (uint64_t k = lo; k < hi; ++k) {
                 const uint64_t a = i0 + k * blk, e = std::min(i0 + nc, a + blk);
                 uint64_t o = bo[k];
-                auto src_of = [&](uint64_t i) {
-                    const uint64_t g = rg[i], r = (uint64_t)ids[i] - g * G;
-                    return src_base + goff[g] + r * rrb[i];
-                };
+                auto src_of = [&](uint64_t i) { return src_base + rsrc[i]; };
                 for (uint64_t i = a; i < std::min(e, a + kAhead); ++i) {
                     const uint8_t *p = src_of(i);
                     for (uint32_t c = 0; c < rrb[i]; c += 64) __builtin_prefetch(p + c);
@@ -321,12 +338,12 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
         });
         h->stats.host_pack_ns +=
             (uint64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(std::chrono::steady_clock::now() - t0).count();
-        const uint64_t total = 8 * nc + total_pay;
+        const uint64_t total = tables + total_pay;
         IBP_HIP(h, hipMemcpyAsync(h->d_stage[b], stg, total, hipMemcpyHostToDevice, h->copy_stream));
         IBP_HIP(h, hipEventRecord(h->ev_copied[b], h->copy_stream));
         IBP_HIP(h, hipStreamWaitEvent(s, h->ev_copied[b], 0));
         const uint8_t *dst = h->d_stage[b];
-        IBP_HIP(h, dev::launch_gather(h->ds, dst + 8 * nc, nullptr, reinterpret_cast<const uint32_t *>(dst),
+        IBP_HIP(h, dev::launch_gather(h->ds, dst + tables, nullptr, reinterpret_cast<const uint32_t *>(dst),
                                       reinterpret_cast<const uint32_t *>(dst) + nc, nc, d_out + i0 * L, h->d_err, s));
         IBP_HIP(h, hipEventRecord(h->ev_free[b], s));
         h->stage_used[b] = true;
@@ -376,13 +393,14 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
         return s;
     };
     const uint64_t meta_bytes = d.n_groups * 2ull * d.row_bytes;
+    const uint64_t n_index = (d.flags & IBP_STREAM_PARTICIPATION) ? d.n_rows + 1 : d.n_groups + 1;
     if (hipMalloc((void **)&h->d_meta, std::max<uint64_t>(meta_bytes, 4)) != hipSuccess ||
-        hipMalloc((void **)&h->d_index, 8 * (d.n_groups + 1)) != hipSuccess ||
+        hipMalloc((void **)&h->d_index, 8 * n_index) != hipSuccess ||
         hipMalloc((void **)&h->d_err, 8) != hipSuccess)
         return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
     if (meta_bytes && hipMemcpy(h->d_meta, v.meta(), meta_bytes, hipMemcpyHostToDevice) != hipSuccess)
         return bail(fail(IBP_EHIP, "metadata upload failed"));
-    if (hipMemcpy(h->d_index, v.index_bytes(), 8 * (d.n_groups + 1), hipMemcpyHostToDevice) != hipSuccess ||
+    if (hipMemcpy(h->d_index, v.index_bytes(), 8 * n_index, hipMemcpyHostToDevice) != hipSuccess ||
         hipMemset(h->d_err, 0, 8) != hipSuccess)
         return bail(fail(IBP_EHIP, "index upload failed"));
     if (flags == IBP_OPEN_PAYLOAD_DEVICE) {
@@ -413,6 +431,7 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     h->ds.n_rows = d.n_rows;
     h->ds.n_groups = d.n_groups;
     h->ds.g_magic = dev::div_magic(d.group_rows);
+    h->ds.part_m = (d.flags & IBP_STREAM_PARTICIPATION) ? d.chunk_bytes / 4 : 0;
     h->ds.W = d.row_bytes / 4;
     h->ds.G = d.group_rows;
     ignore(hipSetDevice(prev));
@@ -441,7 +460,9 @@ ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, vo
         // rows of any row range are one contiguous byte range of the payload (clusters back
         // to back, rows of a cluster back to back), so exactly those bytes cross PCIe and
         // the kernel addresses them relative to the chunk's first byte
+        const bool part = d.flags & IBP_STREAM_PARTICIPATION;
         auto row_byte = [&](uint64_t r) {
+            if (part) return h->h_off[r];
             const uint64_t g = std::min(r / G, d.n_groups - 1);
             return h->h_off[g] + (r - g * G) * h->h_rb[g];
         };
