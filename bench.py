@@ -74,18 +74,21 @@ def wk_for(W):
     return 1 if W <= 64 else 2 if W <= 128 else 4 if W <= 256 else 8
 
 
-def kernel_name(workload, W):
+def kernel_name(workload, W, part=False):
     k = wk_for(W)
+    if part:
+        maxr = {1: 4, 2: 4, 4: 2, 8: 1}[k]
+        return f"k_part_rows<{k},{maxr},{'ids' if workload in GATHERS else 'range'}>"
     if workload in GATHERS:
         rb = {1: 8, 2: 4, 4: 2, 8: 1}[k]
         return f"k_gather_rows<{k},{rb}>" if W <= 512 else "k_gather_tiled"
     return f"k_decompress<{k},{ {1: 4, 2: 4, 4: 2, 8: 1}[k] }>"
 
 
-def measured_traffic(workload):
+def measured_traffic(workload, part=False):
     """HBM bytes per launch from the committed rocprofv3 counter summary of this workload,
     or None when the kernel source has changed since the counters were taken."""
-    kind = "k_gather_rows" if workload in GATHERS else "k_decompress"
+    kind = "k_part_rows" if part else "k_gather_rows" if workload in GATHERS else "k_decompress"
     path = os.path.join(ROOT, "profiles", f"{kind}_{workload}.md")
     if not os.path.exists(path):
         return None
@@ -166,14 +169,51 @@ def host_info():
     return {"cpu_model": model, "nproc": len(os.sched_getaffinity(0))}
 
 
+class Layout:
+    """Packed sizes and addressing of a stream, for the algorithmic byte counts: the
+    clustered scheme (a u64 offset per cluster, one packed size per cluster) or the
+    participation scheme (a u64 offset per row, sizes per row)."""
+
+    def __init__(self, stream, d):
+        self.L, self.G = d["row_bytes"], d["group_rows"]
+        self.part = d["flags"] == 1
+        n_index = d["n_rows"] + 1 if self.part else d["n_groups"] + 1
+        self.index = stream[d["index_off"]:d["index_off"] + 8 * n_index].view(np.uint64).astype(np.int64)
+        if self.part:
+            self.row_size = np.diff(self.index)
+        else:
+            n_in_group = np.full(d["n_groups"], self.G, np.int64)
+            n_in_group[-1] = d["n_rows"] - self.G * (d["n_groups"] - 1)
+            self.rb_of_group = np.diff(self.index) // n_in_group
+
+    def sizes(self, ids):
+        return self.row_size[ids] if self.part else self.rb_of_group[ids // self.G]
+
+    def range_bytes(self, f, n):
+        if self.part:
+            return int(self.index[f + n] - self.index[f])
+        return int(self.index[(f + n - 1) // self.G + 1] - self.index[f // self.G])
+
+    def gather_alg(self, ids):
+        """ids, packed rows read, rows written, and per touched cluster its Mask/Bitval
+        (plus its index entry; per row two index entries in the participation scheme)."""
+        clusters = np.unique(ids // self.G).size
+        idx = 16 * ids.size if self.part else 8 * clusters
+        return int(ids.size * 8 + self.sizes(ids).sum() + ids.size * self.L + clusters * 2 * self.L + idx)
+
+    def range_alg(self, f, n):
+        g0, g1 = f // self.G, (f + n - 1) // self.G + 1
+        idx = 8 * (n + 1) if self.part else 8 * (g1 - g0)
+        return int(self.range_bytes(f, n) + n * self.L + (g1 - g0) * 2 * self.L + idx)
+
+
 class Steps:
     """The per-step units of a workload: row-id batches (gathers) or row ranges (streams),
     with the algorithmic HBM bytes one launch over each must move."""
 
-    def __init__(self, workload, cfg, n_steps, index, rb_of_group):
+    def __init__(self, workload, cfg, n_steps, layout):
         from workloads import dlrm_batch_ids, gnn_batch_ids
         self.workload, self.cfg = workload, cfg
-        G, L = cfg.group_rows, cfg.row_bytes
         if workload in GATHERS:
             distinct = min(n_steps, {"gnn_gather": 64, "dlrm": 8, "big_gnn": 8}[workload])
             x = cfg.extra
@@ -183,17 +223,12 @@ class Steps:
             else:
                 self.units = [gnn_batch_ids(cfg.n_rows, x["seeds"], x["fanouts"], batch_index=b)
                               for b in range(distinct)]
-            # ids, packed rows read, rows written, and Mask/Bitval + index entry per cluster
-            self.alg = [int(u.size * 8 + rb_of_group[u // G].sum() + u.size * L + np.unique(u // G).size * (2 * L + 8))
-                        for u in self.units]
+            self.alg = [layout.gather_alg(u) for u in self.units]
             self.rows = [u.size for u in self.units]
         else:
             per = cfg.extra["rows_per_layer"] if workload == "kv_bf16" else cfg.n_rows
             self.units = [(f, per) for f in range(0, cfg.n_rows, per)]
-            self.alg = []
-            for f, n in self.units:
-                g0, g1 = f // G, (f + n - 1) // G + 1
-                self.alg.append(int(index[g1] - index[g0] + n * L + (g1 - g0) * (2 * L + 8)))
+            self.alg = [layout.range_alg(f, n) for f, n in self.units]
             self.rows = [n for _, n in self.units]
 
     def __len__(self):
@@ -204,10 +239,12 @@ class Steps:
         return u if self.workload in GATHERS else np.arange(u[0], u[0] + u[1], dtype=np.int64)
 
 
-def cpu_baseline(stream, rows, steps, last, L, G, seconds):
+def cpu_baseline(stream, rows, steps, last, L, G, seconds, compress_kw=None):
     """The oracle on this host's cores (one thread): decode of exactly the rows of whole
     steps, starting with the step the GPU ran last, until about `seconds` have passed; then
-    compress of the leading clusters of the tensor for about a third of that time."""
+    compress of the leading clusters of the tensor for about a third of that time (with
+    the stream's own scheme: compress_kw holds the participation-scheme parameters)."""
+    kw = compress_kw or {}
     import oracle
     t0 = time.perf_counter()
     done_rows, done_steps, k = 0, 0, last
@@ -224,12 +261,12 @@ def cpu_baseline(stream, rows, steps, last, L, G, seconds):
     # compress: leading clusters, sized from a first cluster's time
     n_groups = (rows.shape[0] + G - 1) // G
     t = time.perf_counter()
-    oracle.compress(rows[:G], G)
+    oracle.compress(rows[:G], G, **kw)
     per_group = max(time.perf_counter() - t, 1e-6)
     ng = int(min(n_groups, max(1, seconds / 3 / per_group)))
     m = min(rows.shape[0], ng * G)
     t = time.perf_counter()
-    oracle.compress(rows[:m], G)
+    oracle.compress(rows[:m], G, **kw)
     comp_s = time.perf_counter() - t
     log(f"[bench] cpu oracle: decode {done_rows * L / dec_s / 1e6:.1f} MB/s over {done_steps} step(s); "
         f"compress {m * L / comp_s / 1e6:.1f} MB/s over {ng} of {n_groups} clusters")
@@ -241,7 +278,7 @@ def cpu_baseline(stream, rows, steps, last, L, G, seconds):
             "host": host_info()}
 
 
-def pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, G, rb_of_group, index):
+def pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, layout):
     """The PCIe-inclusive legs (never `value`): the same steps with the payload in pinned
     host memory, (a) through host-packed staging + DMA on a side stream (host packing of
     the requested rows for gathers, whole cluster ranges for streams) and (b) read by the
@@ -256,10 +293,10 @@ def pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, G, rb_of_group, i
     needs = {}
     for k in set(sel):
         if steps.workload in GATHERS:
-            needs[k] = int(rb_of_group[steps.units[k] // G].sum()) + 8 * steps.rows[k]
+            needs[k] = int(layout.sizes(steps.units[k]).sum()) + 8 * steps.rows[k]
         else:
             f, n = steps.units[k]
-            needs[k] = int(index[(f + n - 1) // G + 1] - index[f // G])
+            needs[k] = layout.range_bytes(f, n)
     need = sum(needs[k] for k in sel)
     cr = out_total / need
 
@@ -417,6 +454,14 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-e2e", action="store_true")
     ap.add_argument("--e2e-steps", type=int, default=20)
+    ap.add_argument("--scheme", default="clustered", choices=["clustered", "participation"],
+                    help="clustered: Mask/Bitval per cluster of the workload's G rows with T = G (the default); "
+                         "participation: the thresholded scheme with participation bits")
+    ap.add_argument("--chunk-bytes", type=int, default=8, help="participation scheme: chunk bytes")
+    ap.add_argument("--threshold", default="4/5", help="participation scheme: T/N as num/den")
+    ap.add_argument("--mask-rows", type=int, default=0,
+                    help="participation scheme: rows per Mask (0 = one global Mask for all rows)")
+    ap.add_argument("--sample-every", type=int, default=1, help="participation scheme: count every k-th row")
     ap.add_argument("--micro", action="store_true",
                     help="run the decompression-overhead microbenchmark instead (one JSON line with every point)")
     ap.add_argument("--micro-tensors", type=int, default=100000)
@@ -447,17 +492,21 @@ def main():
     log(f"[bench] {wl}: generated {cfg.n_rows} x {L} B rows in {time.time() - t:.1f}s")
     t = time.time()
     threads = min(16, os.cpu_count() or 1)
-    stream = ibp.ibp_compress(rows, G, n_threads=threads)
+    part = args.scheme == "participation"
+    if part:
+        num, den = (int(x) for x in args.threshold.split("/"))
+        mask_rows = args.mask_rows or cfg.n_rows
+        stream = ibp.ibp_compress_ex(rows, mask_rows, args.chunk_bytes, (num, den), args.sample_every,
+                                     n_threads=threads)
+    else:
+        stream = ibp.ibp_compress(rows, G, n_threads=threads)
     compress_s = time.time() - t
     d = ibp.ibp_describe(stream)
-    index = stream[d["index_off"]:d["index_off"] + 8 * (d["n_groups"] + 1)].view(np.uint64).astype(np.int64)
-    n_in_group = np.full(d["n_groups"], G, np.int64)
-    n_in_group[-1] = cfg.n_rows - G * (d["n_groups"] - 1)
-    rb_of_group = np.diff(index) // n_in_group
+    layout = Layout(stream, d)
     log(f"[bench] compressed in {compress_s:.2f}s ({threads} threads): payload {d['payload_bytes'] / 1e6:.1f} MB, "
         f"stream {d['stream_bytes'] / 1e6:.1f} MB, raw {cfg.n_rows * L / 1e6:.1f} MB")
 
-    steps = Steps(wl, cfg, Wm + K, index, rb_of_group)
+    steps = Steps(wl, cfg, Wm + K, layout)
     out = torch.empty(max(steps.rows) * L, dtype=torch.uint8, device="cuda")
     h = ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_DEVICE)
     if wl in GATHERS:
@@ -514,19 +563,21 @@ def main():
     log(f"[bench] same steps over uncompressed rows (device-resident): {out_bytes / wall_u / 1e9:.1f} GB/s "
         f"-> compressed is {wall_u / wall:.2f}x the uncompressed speed")
     copy_gbs = d2d_copy_gbs(torch)
-    traffic = measured_traffic(wl)
+    traffic = measured_traffic(wl, part)
     log(f"[bench] {K} steps in {wall * 1e3:.2f} ms: {value:.1f} GB/s decompressed; kernel {kern_ms * 1e3:.1f} us "
         f"avg, {achieved:.0f} GB/s algorithmic ({achieved / HBM_PEAK_GBS:.1%} of HBM peak); "
         f"plain 1 GiB d2d copy {copy_gbs:.0f} GB/s")
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(stream, rows, steps, last, L, G, args.cpu_seconds)
+        kw = ({"chunk_bytes": args.chunk_bytes, "threshold": (num, den), "sample_every": args.sample_every}
+              if part else None)
+        cpu = cpu_baseline(stream, rows, steps, last, L, G, args.cpu_seconds, kw)
         cpu["host_compressor"] = {"GBps": round(cfg.n_rows * L / compress_s / 1e9, 3), "threads": threads}
 
     e2e = None
     if not args.no_e2e:
-        e2e = pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, G, rb_of_group, index)
+        e2e = pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, layout)
 
     line = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": Wm,
@@ -534,11 +585,15 @@ def main():
         "vs_baseline": None, "dtype": "u32", "data": "synthetic",
         "config": {"workload": DESCRIPTIONS[wl], "rows": cfg.n_rows, "row_bytes": L, "group_rows": G,
                    "rows_per_step_avg": round(float(np.mean(steps.rows)), 1),
+                   "scheme": ({"name": "participation", "chunk_bytes": args.chunk_bytes,
+                               "threshold": args.threshold, "mask_rows": args.mask_rows or cfg.n_rows,
+                               "sample_every": args.sample_every} if part else
+                              {"name": "clustered", "group_rows": G}),
                    "payload_cr": round(cfg.n_rows * L / d["payload_bytes"], 3),
                    "stream_cr": round(cfg.n_rows * L / d["stream_bytes"], 3)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "kernel": kernel_name(wl, W), "kernel_us": round(kern_ms * 1e3, 2),
+                     "kernel": kernel_name(wl, W, part), "kernel_us": round(kern_ms * 1e3, 2),
                      "kernel_us_median": round(float(np.median(kern_all)) * 1e3, 2),
                      "kernel_us_min": round(float(kern_all.min()) * 1e3, 2),
                      "algorithmic_bytes_per_launch": int(alg_avg), "d2d_copy_GBps": round(copy_gbs, 1)},
