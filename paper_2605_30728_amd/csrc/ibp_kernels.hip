@@ -743,11 +743,191 @@ __global__ __launch_bounds__(kBlock) void k_part_rows(DevStream s, const uint32_
     }
 }
 
+// RB participation-scheme rows of one cluster (tile t), one tile each (W <= 64K): the
+// participation dwords of all RB rows are loaded together, then every row's widths, scan
+// and two-dword windows, then the rebuilt words are stored. Loads are unconditional with
+// clamped addresses (inside the row or the readable slack), so no exec-masked load makes
+// earlier loads drain.
+template <int NR, int RB, int K, int MAXR>
+__device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                           const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
+                                           const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
+                                           uint32_t C, uint32_t W) {
+    const uint32_t l = lane_id();
+    const uint32_t nd = (((W - 1) / m) >> 5) + 1;
+    const uint32_t ql = min(l, nd - 1);
+    uint32_t pd[RB];
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+        const uint32_t *__restrict__ p = pay32 + (rbyte[u] >> 2);
+        pd[u] = __builtin_amdgcn_alignbit(p[ql + 1], p[ql], ((uint32_t)rbyte[u] & 3u) * 8u);
+    }
+    uint32_t d0[RB][K], d1[RB][K], b[RB][K], pb[RB][K];
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+        uint32_t width[K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t w = l + kWave * j;
+            const uint32_t c = (w < W ? w : 0u) / m;
+            const uint32_t dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((c >> 5) & 63u) * 4u), (int)pd[u]);
+            pb[u][j] = raw[u] ? 0u : (dw >> (c & 31u)) & 1u;
+            width[j] = w < W ? (pb[u][j] ? (uint32_t)__builtin_popcount(t.nm[j]) : 32u) : 0u;
+        }
+        const uint32_t *__restrict__ p = pay32 + (rbyte[u] >> 2);
+        const uint32_t start = ((uint32_t)rbyte[u] & 3u) * 8u + (raw[u] ? 0u : C);
+        uint32_t c = 0;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t inc = wave_incl_scan(width[j]);
+            b[u][j] = start + c + inc - width[j];
+            c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+            d0[u][j] = p[b[u][j] >> 5];
+            d1[u][j] = p[(b[u][j] >> 5) + 1];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t x = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], b[u][j]);
+            uint32_t v;
+            if constexpr (NR >= 0) v = word_fast<NR>(t, j, x);
+            else v = word_generic(t.bv[j], t.nm[j], x);
+            v = pb[u][j] ? v : x;
+            const uint32_t w = l + kWave * j;
+            if (ok[u] && w < W) orow[u][w] = v;
+        }
+    }
+}
+
+template <int RB, int K, int MAXR>
+__device__ __forceinline__ void part_batch_any(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                               const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
+                                               const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
+                                               uint32_t C, uint32_t W) {
+    switch (t.nr) {   // wave-uniform
+    case 0: part_batch<0, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return;
+    case 1: part_batch<1, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return;
+    case 2: if constexpr (MAXR >= 2) { part_batch<2, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return; } break;
+    case 3: if constexpr (MAXR >= 3) { part_batch<3, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return; } break;
+    case 4: if constexpr (MAXR >= 4) { part_batch<4, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return; } break;
+    default: break;
+    }
+    part_batch<-1, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W);
+}
+
+// Participation-scheme rows that fit one tile (W <= 64K), in batches of RB rows. A wave
+// owns `seg` (<= 64) work items; lane i < seg first locates item i (its cluster, the
+// byte of its row and its size), then batches of RB rows are decoded with part_batch
+// while they share a cluster (always, under one global Mask), else row by row.
+template <int K, int MAXR, int RB, int SRC>
+__global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint32_t *__restrict__ pay32,
+                                                          uint64_t pay_base, const int64_t *__restrict__ ids,
+                                                          const uint32_t *__restrict__ sg,
+                                                          const uint32_t *__restrict__ soff, uint64_t first,
+                                                          uint64_t n, uint32_t *__restrict__ out, uint32_t seg,
+                                                          unsigned long long *err) {
+    const uint64_t i0 = wave_slot() * seg;
+    if (i0 >= n) return;
+    const uint32_t cnt = (uint32_t)min((uint64_t)seg, n - i0);
+    const uint32_t l = lane_id();
+    const uint32_t W = s.W, m = s.part_m, C = W / m;
+    const uint32_t li = l < cnt ? l : cnt - 1;      // lanes past the end repeat the last item
+    uint64_t g_l, byte_l, size_l;
+    bool valid = true;
+    if constexpr (SRC == kSrcStaged) {
+        g_l = sg[i0 + li];
+        byte_l = soff[i0 + li];
+        size_l = soff[i0 + li + 1] - byte_l;
+    } else {
+        uint64_t r;
+        if constexpr (SRC == kSrcIds) {
+            const int64_t id = ids[i0 + li];
+            valid = id >= 0 && (uint64_t)id < s.n_rows;
+            r = valid ? (uint64_t)id : 0u;
+        } else {
+            r = first + i0 + li;
+        }
+        g_l = s.G == 1 ? r : __umul64hi(r, s.g_magic);
+        const uint64_t o0 = s.index[r];
+        byte_l = o0 - pay_base;
+        size_l = s.index[r + 1] - o0;
+    }
+    const uint64_t bad = __ballot(l < cnt && !valid);
+    uint32_t *__restrict__ out_seg = out + i0 * W;
+    if (bad) {
+        for (uint32_t i = 0; i < cnt; ++i)
+            if ((bad >> i) & 1ull)
+                for (uint32_t w = l; w < W; w += kWave) out_seg[(uint64_t)i * W + w] = 0u;
+        if (l == 0) atomicAdd(err, (unsigned long long)__popcll(bad));
+    }
+    auto rd64 = [](uint64_t v, uint32_t i) -> uint64_t {
+        return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), (int)i) << 32) |
+               (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, (int)i);
+    };
+    Tile<K, MAXR> t;
+    uint64_t cached_g = ~0ull;
+    for (uint32_t i = 0; i < cnt; i += RB) {
+        uint64_t rbyte[RB];
+        bool raw[RB], ok[RB];
+        uint32_t *orow[RB];
+        const uint64_t g0 = rd64(g_l, i);
+        bool same = true;
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
+            const uint32_t iu = min(i + u, cnt - 1);
+            rbyte[u] = rd64(byte_l, iu);
+            raw[u] = rd64(size_l, iu) == 4ull * W;
+            ok[u] = i + u < cnt && !((bad >> iu) & 1ull);
+            orow[u] = out_seg + (uint64_t)iu * W;
+            same = same && rd64(g_l, iu) == g0;
+        }
+        if (same) {
+            if (g0 != cached_g) {
+                tile_setup(t, s.meta + g0 * 2ull * W, W, 0, 0);
+                cached_g = g0;
+            }
+            part_batch_any<RB>(t, pay32, rbyte, raw, ok, orow, m, C, W);
+        } else {
+#pragma unroll
+            for (int u = 0; u < RB; ++u) {
+                if (!ok[u]) continue;
+                const uint64_t gu = rd64(g_l, i + u);
+                if (gu != cached_g) {
+                    tile_setup(t, s.meta + gu * 2ull * W, W, 0, 0);
+                    cached_g = gu;
+                }
+                part_tile_any(t, pay32, rbyte[u], raw[u], m, raw[u] ? 0u : C, W, 0, orow[u]);
+            }
+        }
+    }
+}
+
 template <int K, int MAXR>
 hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_base, const int64_t *ids,
                          const uint32_t *sg, const uint32_t *soff, uint64_t first, uint64_t n, uint32_t *o,
                          unsigned long long *err, hipStream_t stream) {
-    // about 16k waves when there is enough work, at most 16 rows per wave
+    if (s.W <= (uint32_t)(kWave * K)) {
+        // rows of one tile: batches of RB rows, 1-4 batches per wave (more when there is
+        // work for ~16k waves, so a wave's tile setup serves more rows)
+        constexpr int RB = K <= 1 ? 8 : (K <= 2 ? 4 : (K <= 4 ? 2 : 1));
+        const uint32_t nb = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(4, n / (16384ull * RB)));
+        const uint32_t seg = RB * nb;
+        const uint64_t waves = (n + seg - 1) / seg;
+        const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
+        if (ids)
+            hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds>), grid, block, 0, stream, s, p, pay_base, ids,
+                               sg, soff, first, n, o, seg, err);
+        else if (sg)
+            hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcStaged>), grid, block, 0, stream, s, p, pay_base,
+                               ids, sg, soff, first, n, o, seg, err);
+        else
+            hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcRange>), grid, block, 0, stream, s, p, pay_base,
+                               ids, sg, soff, first, n, o, seg, err);
+        return hipGetLastError();
+    }
+    // rows of several tiles: one row at a time per wave
     const uint32_t per_wave = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(16, n / 16384));
     const uint64_t waves = (n + per_wave - 1) / per_wave;
     const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
