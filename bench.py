@@ -33,7 +33,8 @@ Also reported on the same JSON line:
 
 `--micro` runs the paper's decompression-overhead microbenchmark instead (tensors of
 256 B / 1 KB / 4 KB at 10-90% space savings, PCIe paths normalised to the mock system)
-and prints one JSON line holding every point.
+and prints one JSON line holding every point. `--cache` compares the compressed device
+cache with an uncompressed one of the same slab bytes (and no cache) on a gather workload.
 """
 import argparse
 import hashlib
@@ -444,6 +445,90 @@ def micro(args):
                       "points": points}), flush=True)
 
 
+def cache_bench(args):
+    """The compressed device cache (Sec. 5, cache compression) on a gather workload: a slab
+    of --cache-frac of the table's raw bytes is filled with the most popular rows (DLRM:
+    by Zipf rank; GNN: most frequent in a profiling pass over batches other than the
+    timed ones), in packed form (about CR times more rows) or uncompressed (rows of a
+    stream whose Masks are all 0); the
+    timed steps gather through ibp_cache_gather, hits decoded from HBM and misses from
+    pinned host memory read in place. Also the same steps with no cache."""
+    import torch
+    import paper_2605_30728_amd as ibp
+    from workloads import CONFIGS, gen_all_rows, gnn_batch_ids
+    wl = args.workload
+    if wl not in GATHERS:
+        log("--cache needs a gather workload")
+        sys.exit(2)
+    cfg = CONFIGS[wl]
+    G, L = cfg.group_rows, cfg.row_bytes
+    K, Wm = args.steps, args.warmup
+    rows = gen_all_rows(cfg)
+    stream = ibp.ibp_compress(rows, G, n_threads=min(16, os.cpu_count() or 1))
+    d = ibp.ibp_describe(stream)
+    layout = Layout(stream, d)
+    steps = Steps(wl, cfg, Wm + K, layout)
+    x = cfg.extra
+    budget = int(args.cache_frac * cfg.n_rows * L)
+    if wl == "dlrm":
+        # Zipf popularity is known: fill in rank order (what a long profiling pass gives)
+        from workloads import dlrm_hot_order
+        order = dlrm_hot_order(x["tables"], x["rows_per_table"], n=min(cfg.n_rows, 8 * budget // L))
+    else:
+        prof = range(1000, 1000 + args.cache_profile_batches)
+        prof_ids = [gnn_batch_ids(cfg.n_rows, x["seeds"], x["fanouts"], batch_index=b) for b in prof]
+        counts = np.bincount(np.concatenate(prof_ids), minlength=cfg.n_rows)
+        order = np.argsort(-counts, kind="stable")
+    csum = np.cumsum(layout.sizes(order))
+    n_comp = int(np.searchsorted(csum, budget, side="right"))
+    n_raw = budget // L
+    log(f"[cache] {wl}: slab budget {budget / 1e6:.1f} MB = {n_comp} packed rows or {n_raw} raw rows")
+    d_units = [torch.from_numpy(u).cuda() for u in steps.units]
+    out = torch.empty(max(steps.rows) * L, dtype=torch.uint8, device="cuda")
+    out_bytes = sum(steps.rows[(Wm + k) % len(steps)] * L for k in range(K))
+    last = (Wm + K - 1) % len(steps)
+
+    def timed(fn):
+        for k in range(Wm):
+            fn(k)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for k in range(K):
+            fn(Wm + k)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t
+        got = out[:steps.rows[last] * L].cpu().numpy().reshape(-1, L)
+        assert np.array_equal(got, rows[steps.row_ids(last)]), "cache gather output"
+        return out_bytes / dt / 1e9
+
+    res = {}
+    for name, src, n_cached in (("compressed", stream, n_comp), ("uncompressed", None, n_raw)):
+        if src is None:
+            src = identity_stream(rows, G)
+        h = ibp.ibp_open(src, 0, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)
+        del src
+        c = ibp.ibp_cache_create(h, order[:n_cached])
+        gbs = timed(lambda k: ibp.ibp_cache_gather(c, d_units[k % len(steps)], out))
+        st = ibp.ibp_cache_get_stats(c)
+        hit = st["hits"] / max(1, st["hits"] + st["misses"])
+        res[name] = {"GBps": round(gbs, 2), "hit_rate": round(hit, 4), "rows_cached": st["rows"],
+                     "slab_bytes": st["slab_bytes"]}
+        log(f"[cache] {name}: {st['rows']} rows in {st['slab_bytes'] / 1e6:.1f} MB, hit rate {hit:.3f}, "
+            f"{gbs:.1f} GB/s decompressed")
+        if name == "compressed":
+            gbs0 = timed(lambda k: ibp.ibp_gather_decompress_device(h, d_units[k % len(steps)], out))
+            res["no_cache"] = {"GBps": round(gbs0, 2), "hit_rate": 0.0}
+            log(f"[cache] no cache (zero-copy gather): {gbs0:.1f} GB/s")
+        ibp.ibp_cache_destroy(c)
+        ibp.ibp_close(h)
+    print(json.dumps({"metric": "compressed device cache: decompressed GB/s and hit rate at equal slab bytes",
+                      "value": res["compressed"]["GBps"], "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": Wm,
+                      "data": "synthetic", "config": {"workload": DESCRIPTIONS[wl], "cache_frac": args.cache_frac,
+                                                      "slab_budget_bytes": budget,
+                                                      "profile_batches": args.cache_profile_batches},
+                      "variants": res}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -462,6 +547,10 @@ def main():
     ap.add_argument("--mask-rows", type=int, default=0,
                     help="participation scheme: rows per Mask (0 = one global Mask for all rows)")
     ap.add_argument("--sample-every", type=int, default=1, help="participation scheme: count every k-th row")
+    ap.add_argument("--cache", action="store_true",
+                    help="run the compressed device cache comparison on a gather workload instead")
+    ap.add_argument("--cache-frac", type=float, default=0.05, help="slab bytes as a fraction of the raw table")
+    ap.add_argument("--cache-profile-batches", type=int, default=32)
     ap.add_argument("--micro", action="store_true",
                     help="run the decompression-overhead microbenchmark instead (one JSON line with every point)")
     ap.add_argument("--micro-tensors", type=int, default=100000)
@@ -477,6 +566,9 @@ def main():
         sys.exit(2)
     if args.micro:
         micro(args)
+        return
+    if args.cache:
+        cache_bench(args)
         return
 
     import torch

@@ -243,9 +243,57 @@ ibp_status ibp_reset_stats(ibp_handle *h);
 /*
  * ibp_close -- wait for the handle's outstanding work, free everything it owns and
  * invalidate it. NULL is accepted (IBP_OK). Closing twice is undefined: the handle
- * memory is freed by the first close.
+ * memory is freed by the first close. IBP_ESTATE while caches built on it exist.
  */
 ibp_status ibp_close(ibp_handle *h);
+
+/*
+ * Compressed device-resident row cache (Sec. 5, cache compression). A static set of
+ * rows is kept on the device in packed form, back to back in one data slab, so a slab of
+ * B bytes holds about CR times more rows than an uncompressed cache; a lookup table
+ * maps a row id to a 64-bit entry: slab byte offset (bits 0-39), slab id (bits 40-42,
+ * always 0 on one GPU), compressed-form flag (bit 43; set for every row of a
+ * clustered-scheme stream), bits 44-63 spare. A cache gather decodes hits from the slab
+ * in HBM and misses from the handle's pinned payload, read in place over PCIe, in one
+ * kernel. The cache keeps the handle's metadata on the device as its decode state.
+ */
+typedef struct ibp_cache ibp_cache;   /* opaque, owned by the library */
+
+typedef struct {
+    uint64_t rows;           /* distinct rows held */
+    uint64_t slab_bytes;     /* packed bytes held (the slab) */
+    uint64_t table_slots;    /* lookup table slots (16 bytes each) */
+    uint64_t hits;           /* requests served from the slab since creation or reset */
+    uint64_t misses;         /* requests served from host memory */
+} ibp_cache_stats;
+
+/*
+ * ibp_cache_create -- build a cache holding rows row_ids[0..n_ids) (host memory, read
+ * before the call returns; duplicates are held once) of a handle opened with
+ * IBP_OPEN_PAYLOAD_HOST_ZERO_COPY on a clustered-scheme stream (flags = 0) of at most
+ * 2048-byte rows. Synchronous. The handle must outlive the cache (ibp_close returns
+ * IBP_ESTATE while caches exist).
+ * Errors: IBP_EINVAL (null pointers, another placement or scheme, rows too wide),
+ * IBP_ERANGE (an id out of range), IBP_ENOMEM, IBP_EHIP, IBP_ESTATE.
+ */
+ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, ibp_cache **c);
+
+/*
+ * ibp_cache_gather -- d_out[i] = row(d_row_ids[i]) for i < n_ids (device ids, device
+ * output of n_ids * row_bytes bytes) on `stream`; hits are decoded from the slab, misses
+ * from host memory. An id out of range gives a zero row and counts in
+ * ibp_device_errors() of the handle.
+ * Errors: IBP_EINVAL, IBP_ENOMEM (out_cap too small), IBP_EHIP, IBP_ESTATE.
+ */
+ibp_status ibp_cache_gather(ibp_cache *c, const int64_t *d_row_ids, uint64_t n_ids, void *d_out,
+                            uint64_t out_cap, void *stream);
+
+/* ibp_cache_get_stats -- synchronize the device and copy the cache's sizes and counters. */
+ibp_status ibp_cache_get_stats(ibp_cache *c, ibp_cache_stats *st);
+/* ibp_cache_reset_stats -- synchronize the device and zero the hit / miss counters. */
+ibp_status ibp_cache_reset_stats(ibp_cache *c);
+/* ibp_cache_destroy -- wait for outstanding work and free the cache. NULL is accepted. */
+ibp_status ibp_cache_destroy(ibp_cache *c);
 
 /* ibp_last_error -- message of the last failed call on this thread ("" if none). */
 const char *ibp_last_error(void);

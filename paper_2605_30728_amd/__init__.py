@@ -59,6 +59,14 @@ class ibp_stats(ctypes.Structure):
         return {k: getattr(self, k) for k, _ in self._fields_}
 
 
+class ibp_cache_stats(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_uint64), ("slab_bytes", ctypes.c_uint64), ("table_slots", ctypes.c_uint64),
+                ("hits", ctypes.c_uint64), ("misses", ctypes.c_uint64)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
 _lib = None
 _vp, _u64, _u32, _i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int
 _SIGS = {
@@ -75,6 +83,11 @@ _SIGS = {
     "ibp_get_stats": [_vp, ctypes.POINTER(ibp_stats)],
     "ibp_reset_stats": [_vp],
     "ibp_close": [_vp],
+    "ibp_cache_create": [_vp, _vp, _u64, ctypes.POINTER(_vp)],
+    "ibp_cache_gather": [_vp, _vp, _u64, _vp, _u64, _vp],
+    "ibp_cache_get_stats": [_vp, ctypes.POINTER(ibp_cache_stats)],
+    "ibp_cache_reset_stats": [_vp],
+    "ibp_cache_destroy": [_vp],
 }
 EXPORTS = sorted(list(_SIGS) + ["ibp_last_error", "ibp_version"])
 
@@ -267,5 +280,53 @@ def ibp_reset_stats(h):
 
 def ibp_close(h):
     if h.ptr:
-        p, h.ptr = h.ptr, None
-        _check(lib().ibp_close(p), "ibp_close")
+        st = lib().ibp_close(h.ptr)
+        if st != IBP_ESTATE:      # the handle is freed on every other outcome
+            h.ptr = None
+        _check(st, "ibp_close")
+
+
+class Cache:
+    """A compressed device cache (ibp_cache*). Destroy with ibp_cache_destroy(c) or use as
+    a context manager."""
+
+    def __init__(self, ptr, handle):
+        self.ptr = ptr
+        self.handle = handle
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        ibp_cache_destroy(self)
+
+
+def ibp_cache_create(h, row_ids):
+    ids = np.ascontiguousarray(row_ids, dtype=np.int64)
+    c = _vp(0)
+    _check(lib().ibp_cache_create(h.ptr, ids.ctypes.data, ids.size, ctypes.byref(c)), "ibp_cache_create")
+    return Cache(c.value, h)
+
+
+def ibp_cache_gather(c, d_row_ids, d_out, n_ids=None, out_cap=None, stream=None):
+    n = d_row_ids.numel() if n_ids is None else n_ids
+    cap = _nbytes(d_out) if out_cap is None else out_cap
+    _check(lib().ibp_cache_gather(c.ptr, _ptr(d_row_ids), n, _ptr(d_out), cap, _stream(stream)), "ibp_cache_gather")
+
+
+def ibp_cache_get_stats(c):
+    st = ibp_cache_stats()
+    _check(lib().ibp_cache_get_stats(c.ptr, ctypes.byref(st)), "ibp_cache_get_stats")
+    return st.as_dict()
+
+
+def ibp_cache_reset_stats(c):
+    _check(lib().ibp_cache_reset_stats(c.ptr), "ibp_cache_reset_stats")
+
+
+def ibp_cache_destroy(c):
+    if c.ptr:
+        st = lib().ibp_cache_destroy(c.ptr)
+        if st != IBP_ESTATE:      # the cache is freed on every other outcome
+            c.ptr = None
+        _check(st, "ibp_cache_destroy")

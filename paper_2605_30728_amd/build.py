@@ -17,7 +17,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libibp.so")
 ARCH = os.environ.get("IBP_OFFLOAD_ARCH", "gfx950")
 
-HIP_SOURCES = ["ibp_kernels.hip", "ibp_runtime.hip"]
+HIP_SOURCES = ["ibp_kernels.hip", "ibp_cache_kernels.hip", "ibp_runtime.hip"]
 CXX_SOURCES = ["ibp_host.cpp", "ibp_pool.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]

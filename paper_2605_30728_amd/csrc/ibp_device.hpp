@@ -40,5 +40,25 @@ hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64
                          const uint32_t *sg, const uint32_t *soff, uint64_t n, void *out,
                          unsigned long long *err, hipStream_t stream);
 
+// Hit / miss counters of a cache: kCountLines pairs, one per 128-byte line.
+inline constexpr uint32_t kCountLines = 64;
+inline constexpr uint32_t kCountStride = 16;   // u64 per line
+
+// A compressed row cache resident on the device (see ibp_cache_kernels.hip).
+struct CacheView {
+    const void *table;               // 2^log2cap slots of {u64 key = id + 1 (0 empty), u64 entry}
+    const uint8_t *slab;             // cached packed rows (readable 8 bytes past the last)
+    const uint8_t *host_payload;     // device address of the pinned payload (misses)
+    unsigned long long *counts;      // kCountLines x [hits, misses, unused...]
+    uint64_t mask;                   // 2^log2cap - 1
+    uint32_t log2cap;
+};
+
+// out[i] = row ids[i] for a clustered-scheme stream of at most 512 words per row: rows
+// found in the cache table are decoded from the slab, the others from the pinned host
+// payload; ids outside [0, n_rows) give a zero row and one increment of *err.
+hipError_t launch_cache_gather(const DevStream &s, const CacheView &c, const int64_t *ids, uint64_t n, void *out,
+                               unsigned long long *err, hipStream_t stream);
+
 }  // namespace dev
 }  // namespace ibp

@@ -25,35 +25,13 @@
 #include <algorithm>
 
 #include "ibp_device.hpp"
+#include "ibp_wave.hpp"
 
 namespace ibp {
 namespace dev {
 
 namespace {
 
-constexpr int kWave = 64;
-constexpr int kWavesPerBlock = 4;
-constexpr int kBlock = kWave * kWavesPerBlock;
-
-__device__ __forceinline__ uint32_t lane_id() { return __lane_id(); }
-
-// Inclusive prefix sum over the 64 lanes of a wave: row_shr 1/2/4/8 scan each row of
-// 16 lanes, row_bcast:15 carries rows 0->1 and 2->3, row_bcast:31 carries rows 0-1
-// into rows 2-3. Disabled or out-of-row sources contribute 0 (old value 0).
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
-    int x = (int)v;
-    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);  // row_shr:1
-    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);  // row_shr:2
-    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);  // row_shr:4
-    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);  // row_shr:8
-    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);  // row_bcast:15
-    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);  // row_bcast:31
-    return (uint32_t)x;
-}
-
-__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
-    return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(v), 63);
-}
 
 // Per-wave decode state for one tile of a row (64*K words) of one cluster.
 template <int K, int MAXR>
@@ -258,10 +236,6 @@ __device__ __forceinline__ void decode_rows_tiled(const uint32_t *__restrict__ m
     }
 }
 
-__device__ __forceinline__ uint64_t wave_slot() {
-    return (uint64_t)blockIdx.x * kWavesPerBlock +
-           (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
-}
 
 // One wave per unit = (cluster, slice of at most rpu rows of it).
 template <int K, int MAXR>
@@ -376,99 +350,6 @@ __global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint
 // issued after a batch's stores would wait for those stores as well). Rows are rebuilt
 // with the generic run walk: with a setup per row, precomputed runs would cost more than
 // they save.
-template <int K>
-struct RowMeta {
-    uint32_t m[K], b[K];
-};
-
-// Raw Mask/Bitval words of the lane's words of a row. Lanes past the row's end load a
-// valid word (clamped address) and are masked where the words are used, so the loads
-// carry no exec mask and no default value that would force earlier loads to drain.
-template <int K>
-__device__ __forceinline__ void load_row_meta(RowMeta<K> &rm, const uint32_t *__restrict__ mg, uint32_t W) {
-    const uint32_t l = lane_id();
-#pragma unroll
-    for (int j = 0; j < K; ++j) {
-        const uint32_t w = min(l + kWave * j, W - 1);
-        rm.m[j] = mg[w];
-        rm.b[j] = mg[W + w];
-    }
-}
-
-// Maximum over the 64 lanes of a wave (DPP, as the scan), result in every lane's SGPR.
-__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
-    int x = (int)v;
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false));  // row_shr:1
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false));  // row_shr:2
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false));  // row_shr:4
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false));  // row_shr:8
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false));  // row_bcast:15
-    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false));  // row_bcast:31
-    return (uint32_t)__builtin_amdgcn_readlane(x, 63);
-}
-
-// Deposit by holes. The variant positions nm of a word span [lo, hi]; inside that span
-// the invariant positions form "holes" (runs of invariant bits). Shifting the packed
-// bits x up to lo places them contiguously; opening a gap of the right width at every
-// hole, lowest first (bits at and above the hole move up by its width), puts each bit on
-// its variant position, and Bitval fills the rest. A word with r runs of variant bits
-// has r - 1 holes.
-__device__ __forceinline__ uint32_t run_count(uint32_t v) { return (uint32_t)__builtin_popcount(v & ~(v << 1)); }
-
-// nh is wave-uniform and at least the word's own hole count; extra iterations find no
-// hole (below = all but bit 31, width 0) and leave y as it is.
-__device__ __forceinline__ uint32_t word_deposit(uint32_t bv, uint32_t nm, uint32_t x, uint32_t nh) {
-    const uint32_t lo = (uint32_t)__builtin_ctz(nm | 0x80000000u);
-    // span [lo, hi] (nm = 0 gives garbage that the final select discards)
-    const uint32_t span = (0xFFFFFFFFu >> __builtin_clz(nm | 1u)) & (0xFFFFFFFFu << lo);
-    uint32_t holes = span & ~nm;   // never holds bit 31: the top of the span is variant
-    uint32_t y = x << lo;
-    for (uint32_t k = 0; k < nh; ++k) {
-        const uint32_t pos = (uint32_t)__builtin_ctz(holes | 0x80000000u);
-        const uint32_t t = holes + (1u << pos);      // carries through the lowest hole
-        const uint32_t width = (uint32_t)__builtin_popcount(holes & ~t);
-        holes &= t;
-        const uint32_t below = (1u << pos) - 1u;
-        y = (y & below) | ((y << width) & ~below);
-    }
-    return (nm & y) | (~nm & bv);
-}
-
-// Exclusive bit offsets of the lane's words inside a packed row (word order t + 64*j)
-// and the row's total packed bits. Two strides share one wave scan: every count is at
-// most 32, so every prefix is at most 2048 and fits a 16-bit field.
-template <int K>
-__device__ __forceinline__ uint32_t row_offsets(const uint32_t (&n)[K], uint32_t (&s)[K]) {
-    uint32_t c = 0;
-#pragma unroll
-    for (int j = 0; j < K; j += 2) {
-        if (j + 1 < K) {
-            const uint32_t v = n[j] | (n[j + 1] << 16);
-            const uint32_t inc = wave_incl_scan(v);
-            const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
-            s[j] = c + (inc & 0xFFFFu) - n[j];
-            c += tot & 0xFFFFu;
-            s[j + 1] = c + (inc >> 16) - n[j + 1];
-            c += tot >> 16;
-        } else {
-            const uint32_t inc = wave_incl_scan(n[j]);
-            s[j] = c + inc - n[j];
-            c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
-        }
-    }
-    return c;
-}
-
-// Blocks are dealt to the 8 XCDs round-robin; renumber them so that consecutive
-// logical blocks (neighbouring sorted ids, which share clusters) run on one XCD and
-// share its L2. A bijection on [0, nblocks) for any nblocks.
-__device__ __forceinline__ uint32_t xcd_block(uint32_t b, uint32_t nblocks) {
-    constexpr uint32_t kXcd = 8;
-    const uint32_t xcd = b % kXcd, idx = b / kXcd;
-    const uint32_t per = nblocks / kXcd, extra = nblocks % kXcd;
-    return xcd * per + min(xcd, extra) + idx;
-}
-
 template <int K, int RB, bool STAGED>
 __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint32_t *__restrict__ pay32,
                                                          const int64_t *__restrict__ ids,

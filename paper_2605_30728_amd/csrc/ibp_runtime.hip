@@ -43,6 +43,7 @@ constexpr uint64_t kSlack = 256;                 // readable bytes past any payl
 constexpr uint64_t kStageBytes = 64ull << 20;    // one staging buffer
 constexpr int kStages = 3;                        // staging buffers in rotation
 constexpr int kIdSlots = 2;                       // host-id buffers in rotation
+constexpr uint64_t kCountBytes = dev::kCountLines * dev::kCountStride * 8;   // cache counters
 constexpr uint64_t kBlk = 256;                    // rows per host packing task (a chunk
                                                   // holds tens of them, for 16 threads)
 
@@ -102,8 +103,21 @@ struct ibp_handle {
     std::vector<uint64_t> chunk_off;       // staged byte offset of every block of one chunk
     Pool *pool = nullptr;
     std::atomic<int> busy{0};
+    int n_caches = 0;                      // live caches built on this handle
     ibp_stats stats{};
     hipError_t sticky = hipSuccess;
+};
+
+// A static compressed row cache on the device (Sec. 5, cache compression): cached rows'
+// packed bytes back to back in one device slab, and an open-addressing table from row id
+// to slab entry. Misses are decoded from the handle's pinned payload, read in place.
+struct ibp_cache {
+    ibp_handle *h = nullptr;
+    uint8_t *d_slab = nullptr;
+    void *d_table = nullptr;
+    unsigned long long *d_counts = nullptr;
+    dev::CacheView view{};
+    uint64_t rows = 0, slab_bytes = 0, slots = 0;
 };
 
 namespace {
@@ -601,12 +615,171 @@ ibp_status ibp_close(ibp_handle *h) {
     int expected = 0;
     if (!h->busy.compare_exchange_strong(expected, 1))
         return fail(IBP_ESTATE, "handle is in use by another thread");
+    if (h->n_caches) {
+        h->busy.store(0);
+        return fail(IBP_ESTATE, "destroy the caches built on this handle first");
+    }
     int prev = 0;
     ignore(hipGetDevice(&prev));
     ignore(hipSetDevice(h->device));
     hipError_t e = hipDeviceSynchronize();
     free_handle(h);
     ignore(hipSetDevice(prev));
+    if (e != hipSuccess) return fail(IBP_EHIP, std::string("pending work failed: ") + hipGetErrorString(e));
+    return IBP_OK;
+}
+
+// ---- compressed device cache ---------------------------------------------------
+
+ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, ibp_cache **out) {
+    clear_error();
+    if (!out) return fail(IBP_EINVAL, "cache output is null");
+    *out = nullptr;
+    CallScope cs(h);
+    ibp_status st = check_handle(h, cs);
+    if (st != IBP_OK) return st;
+    const ibp_desc &d = h->d;
+    if (h->flags != IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)
+        return fail(IBP_EINVAL, "a cache needs a handle opened with IBP_OPEN_PAYLOAD_HOST_ZERO_COPY (misses are read "
+                                "from the pinned payload in place)");
+    if (d.flags != 0) return fail(IBP_EINVAL, "the cache holds clustered-scheme streams (flags = 0)");
+    if (d.row_bytes / 4 > 512) return fail(IBP_EINVAL, "the cache supports rows of at most 2048 bytes");
+    if (n_ids && !row_ids) return fail(IBP_EINVAL, "row ids are null");
+    for (uint64_t i = 0; i < n_ids; ++i)
+        if (row_ids[i] < 0 || (uint64_t)row_ids[i] >= d.n_rows)
+            return fail(IBP_ERANGE, "row id " + std::to_string(row_ids[i]) + " at position " + std::to_string(i) +
+                                        " is outside [0, " + std::to_string(d.n_rows) + ")");
+    std::vector<int64_t> ids(row_ids, row_ids + n_ids);
+    std::sort(ids.begin(), ids.end());
+    ids.erase(std::unique(ids.begin(), ids.end()), ids.end());
+    const uint64_t n = ids.size(), G = d.group_rows;
+    // slab: the cached rows' packed bytes back to back, in id order
+    std::vector<uint64_t> src(n), dst(n + 1);
+    dst[0] = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        const uint64_t id = (uint64_t)ids[i], g = id / G;
+        src[i] = h->h_off[g] + (id - g * G) * h->h_rb[g];
+        dst[i + 1] = dst[i] + h->h_rb[g];
+    }
+    if (dst[n] >= (1ull << 40)) return fail(IBP_EINVAL, "cached rows exceed the 40-bit slab offset");
+    uint32_t log2cap = 6;
+    while ((1ull << log2cap) < 2 * n) ++log2cap;
+    const uint64_t cap = 1ull << log2cap;
+    struct Slot {
+        uint64_t key, val;
+    };
+    std::vector<uint8_t> slab;
+    std::vector<Slot> table;
+    try {
+        slab.assign(dst[n] + kSlack, 0);
+        table.assign(cap, Slot{0, 0});
+    } catch (const std::bad_alloc &) {
+        return fail(IBP_ENOMEM, "host allocation for the cache failed");
+    }
+    h->pool->run(n, 4096, [&](uint64_t lo, uint64_t hi) {
+        for (uint64_t i = lo; i < hi; ++i) std::memcpy(slab.data() + dst[i], h->h_payload + src[i], dst[i + 1] - dst[i]);
+    });
+    for (uint64_t i = 0; i < n; ++i) {
+        const uint64_t id = (uint64_t)ids[i];
+        uint64_t k = (id * 0x9E3779B97F4A7C15ull) >> (64 - log2cap);
+        while (table[k].key != 0) k = (k + 1) & (cap - 1);
+        // entry: slab byte offset (bits 0-39), slab 0 (bits 40-42), compressed form (bit 43)
+        table[k] = Slot{id + 1, dst[i] | (1ull << 43)};
+    }
+    auto *c = new (std::nothrow) ibp_cache();
+    if (!c) return fail(IBP_ENOMEM, "host allocation failed");
+    auto bail = [&](ibp_status e) {
+        ignore(hipFree(c->d_slab));
+        ignore(hipFree(c->d_table));
+        ignore(hipFree(c->d_counts));
+        delete c;
+        return e;
+    };
+    if (hipMalloc((void **)&c->d_slab, slab.size()) != hipSuccess ||
+        hipMalloc(&c->d_table, cap * sizeof(Slot)) != hipSuccess ||
+        hipMalloc((void **)&c->d_counts, kCountBytes) != hipSuccess)
+        return bail(fail(IBP_ENOMEM, "device allocation for the cache failed"));
+    if (hipMemcpy(c->d_slab, slab.data(), slab.size(), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(c->d_table, table.data(), cap * sizeof(Slot), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemset(c->d_counts, 0, kCountBytes) != hipSuccess)
+        return bail(fail(IBP_EHIP, "cache upload failed"));
+    c->h = h;
+    c->rows = n;
+    c->slab_bytes = dst[n];
+    c->slots = cap;
+    c->view.table = c->d_table;
+    c->view.slab = c->d_slab;
+    c->view.host_payload = h->k_payload;
+    c->view.counts = c->d_counts;
+    c->view.mask = cap - 1;
+    c->view.log2cap = log2cap;
+    ++h->n_caches;
+    *out = c;
+    return IBP_OK;
+}
+
+ibp_status ibp_cache_gather(ibp_cache *c, const int64_t *d_row_ids, uint64_t n_ids, void *d_out, uint64_t out_cap,
+                            void *stream) {
+    clear_error();
+    if (!c) return fail(IBP_EINVAL, "cache is null");
+    ibp_handle *h = c->h;
+    CallScope cs(h);
+    ibp_status st = check_handle(h, cs);
+    if (st != IBP_OK) return st;
+    if (n_ids == 0) return IBP_OK;
+    if (!d_row_ids || !d_out) return fail(IBP_EINVAL, "row ids or output is null");
+    if (out_cap / h->d.row_bytes < n_ids) return fail(IBP_ENOMEM, "output capacity too small");
+    IBP_HIP(h, dev::launch_cache_gather(h->ds, c->view, d_row_ids, n_ids, d_out, h->d_err,
+                                        static_cast<hipStream_t>(stream)));
+    h->stats.calls += 1;
+    h->stats.rows_out += n_ids;
+    h->stats.out_bytes += n_ids * h->d.row_bytes;
+    return IBP_OK;
+}
+
+ibp_status ibp_cache_get_stats(ibp_cache *c, ibp_cache_stats *st) {
+    clear_error();
+    if (!c || !st) return fail(IBP_EINVAL, "cache or stats is null");
+    CallScope cs(c->h);
+    ibp_status s = check_handle(c->h, cs);
+    if (s != IBP_OK) return s;
+    unsigned long long counts[dev::kCountLines * dev::kCountStride];
+    IBP_HIP(c->h, hipDeviceSynchronize());
+    IBP_HIP(c->h, hipMemcpy(counts, c->d_counts, kCountBytes, hipMemcpyDeviceToHost));
+    st->rows = c->rows;
+    st->slab_bytes = c->slab_bytes;
+    st->table_slots = c->slots;
+    st->hits = st->misses = 0;
+    for (uint32_t k = 0; k < dev::kCountLines; ++k) {
+        st->hits += counts[k * dev::kCountStride];
+        st->misses += counts[k * dev::kCountStride + 1];
+    }
+    return IBP_OK;
+}
+
+ibp_status ibp_cache_reset_stats(ibp_cache *c) {
+    clear_error();
+    if (!c) return fail(IBP_EINVAL, "cache is null");
+    CallScope cs(c->h);
+    ibp_status s = check_handle(c->h, cs);
+    if (s != IBP_OK) return s;
+    IBP_HIP(c->h, hipDeviceSynchronize());
+    IBP_HIP(c->h, hipMemset(c->d_counts, 0, kCountBytes));
+    return IBP_OK;
+}
+
+ibp_status ibp_cache_destroy(ibp_cache *c) {
+    clear_error();
+    if (!c) return IBP_OK;
+    ibp_handle *h = c->h;
+    CallScope cs(h);
+    if (!cs.ok()) return fail(IBP_ESTATE, "the cache's handle is in use by another thread");
+    hipError_t e = hipDeviceSynchronize();
+    ignore(hipFree(c->d_slab));
+    ignore(hipFree(c->d_table));
+    ignore(hipFree(c->d_counts));
+    --h->n_caches;
+    delete c;
     if (e != hipSuccess) return fail(IBP_EHIP, std::string("pending work failed: ") + hipGetErrorString(e));
     return IBP_OK;
 }

@@ -181,6 +181,18 @@ def dlrm_batch_ids(tables, rows_per_table, batch, s, seed=0, batch_index=0):
     return ids.reshape(-1)
 
 
+def dlrm_hot_order(tables, rows_per_table, seed=0, n=None):
+    """The first n row ids of the DLRM tables in popularity order (rank 0 of every
+    table, then rank 1, ...), through the same per-table permutations as
+    dlrm_batch_ids: the order in which a static cache would be filled from a long
+    profiling pass."""
+    n = tables * rows_per_table if n is None else n
+    ranks = (n + tables - 1) // tables
+    cols = [t * rows_per_table + chunk_rng(seed, P_PERM, t).permutation(rows_per_table)[:ranks]
+            for t in range(tables)]
+    return np.stack(cols, axis=1).reshape(-1)[:n]
+
+
 # ---------------------------------------------------------------- test inputs
 
 _KINDS = ("random", "identical", "zeros", "ones", "onebit", "alternating", "floats",
