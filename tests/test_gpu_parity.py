@@ -339,3 +339,42 @@ def test_kv_full(torch):
     assert np.array_equal(oracle.decode_rows(stream, sample, cfg.row_bytes), rows[sample])
     del rows, stream
     gc.collect()
+
+
+def test_independent_handles_on_threads(torch):
+    """Distinct handles are independent: four host threads, each with its own handle
+    (every placement) and its own HIP stream, gather and decompress concurrently; every
+    result equals the oracle's."""
+    import threading
+    rows = structured_rows("floats", 4000, 256, seed=77)
+    stream = oracle.compress(rows, 32)
+    rng = np.random.default_rng(5)
+    jobs = [(flags, rng.integers(0, 4000, size=3000).astype(np.int64))
+            for flags in (FLAGS["device"], FLAGS["host"], FLAGS["zero_copy"], FLAGS["device"])]
+    wants = [oracle.decode_rows(stream, ids, 256) for _, ids in jobs]
+    results, errors = [None] * len(jobs), []
+    say("[threads] 4 handles on 4 threads")
+
+    def work(k, flags, ids):
+        try:
+            s = torch.cuda.Stream()
+            with ibp.ibp_open(stream, 0, flags) as h:
+                out = torch.empty(ids.size * 256, dtype=torch.uint8, device="cuda")
+                whole = torch.empty(4000 * 256, dtype=torch.uint8, device="cuda")
+                for _ in range(5):
+                    ibp.ibp_gather_decompress(h, ids, out, stream=s)
+                    ibp.ibp_decompress(h, 0, 4000, whole, stream=s)
+                s.synchronize()
+                results[k] = (out.cpu().numpy().reshape(-1, 256), whole.cpu().numpy().reshape(-1, 256))
+        except Exception as e:      # reported by the main thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(k, f, ids)) for k, (f, ids) in enumerate(jobs)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for k in range(len(jobs)):
+        assert np.array_equal(results[k][0], wants[k])
+        assert np.array_equal(results[k][1], rows)
