@@ -23,6 +23,7 @@
 //     two dwords at its bit offset and funnel-shifted (v_alignbit_b32), never with
 //     sub-dword loads. No MFMA anywhere: nothing here is a contraction.
 #include <algorithm>
+#include <type_traits>
 
 #include "ibp_device.hpp"
 #include "ibp_wave.hpp"
@@ -490,6 +491,10 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
 
 enum { kSrcRange = 0, kSrcIds = 1, kSrcStaged = 2 };
 
+// Rows of at most 32 * kPreDwords chunks take their participation dwords together with
+// their lookup (one round trip per wave instead of one per batch).
+constexpr int kPreDwords = 2;
+
 // Decode one tile (words [w0, w0 + 64K)) of one participation-scheme row whose bytes
 // start at byte `rbyte` of pay32; `start` is the bit of the row where this tile's first
 // word begins. Returns the tile's bits.
@@ -629,19 +634,21 @@ __global__ __launch_bounds__(kBlock) void k_part_rows(DevStream s, const uint32_
 // and two-dword windows, then the rebuilt words are stored. Loads are unconditional with
 // clamped addresses (inside the row or the readable slack), so no exec-masked load makes
 // earlier loads drain.
-template <int NR, int RB, int K, int MAXR>
+template <int NR, int RB, bool PRE, int K, int MAXR>
 __device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
                                            const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
                                            const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
-                                           uint32_t C, uint32_t W) {
+                                           uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords]) {
     const uint32_t l = lane_id();
-    const uint32_t nd = (((W - 1) / m) >> 5) + 1;
-    const uint32_t ql = min(l, nd - 1);
     uint32_t pd[RB];
+    if constexpr (!PRE) {
+        const uint32_t nd = (((W - 1) / m) >> 5) + 1;
+        const uint32_t ql = min(l, nd - 1);
 #pragma unroll
-    for (int u = 0; u < RB; ++u) {
-        const uint32_t *__restrict__ p = pay32 + (rbyte[u] >> 2);
-        pd[u] = __builtin_amdgcn_alignbit(p[ql + 1], p[ql], ((uint32_t)rbyte[u] & 3u) * 8u);
+        for (int u = 0; u < RB; ++u) {
+            const uint32_t *__restrict__ p = pay32 + (rbyte[u] >> 2);
+            pd[u] = __builtin_amdgcn_alignbit(p[ql + 1], p[ql], ((uint32_t)rbyte[u] & 3u) * 8u);
+        }
     }
     uint32_t d0[RB][K], d1[RB][K], b[RB][K], pb[RB][K];
 #pragma unroll
@@ -651,7 +658,9 @@ __device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_
         for (int j = 0; j < K; ++j) {
             const uint32_t w = l + kWave * j;
             const uint32_t c = (w < W ? w : 0u) / m;
-            const uint32_t dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((c >> 5) & 63u) * 4u), (int)pd[u]);
+            uint32_t dw;
+            if constexpr (PRE) dw = (c >> 5) ? pds[u][1] : pds[u][0];
+            else dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((c >> 5) & 63u) * 4u), (int)pd[u]);
             pb[u][j] = raw[u] ? 0u : (dw >> (c & 31u)) & 1u;
             width[j] = w < W ? (pb[u][j] ? (uint32_t)__builtin_popcount(t.nm[j]) : 32u) : 0u;
         }
@@ -682,27 +691,27 @@ __device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_
     }
 }
 
-template <int RB, int K, int MAXR>
+template <int RB, bool PRE, int K, int MAXR>
 __device__ __forceinline__ void part_batch_any(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
                                                const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
                                                const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
-                                               uint32_t C, uint32_t W) {
+                                               uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords]) {
     switch (t.nr) {   // wave-uniform
-    case 0: part_batch<0, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return;
-    case 1: part_batch<1, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return;
-    case 2: if constexpr (MAXR >= 2) { part_batch<2, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return; } break;
-    case 3: if constexpr (MAXR >= 3) { part_batch<3, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return; } break;
-    case 4: if constexpr (MAXR >= 4) { part_batch<4, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W); return; } break;
+    case 0: part_batch<0, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return;
+    case 1: part_batch<1, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return;
+    case 2: if constexpr (MAXR >= 2) { part_batch<2, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return; } break;
+    case 3: if constexpr (MAXR >= 3) { part_batch<3, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return; } break;
+    case 4: if constexpr (MAXR >= 4) { part_batch<4, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return; } break;
     default: break;
     }
-    part_batch<-1, RB>(t, pay32, rbyte, raw, ok, orow, m, C, W);
+    part_batch<-1, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds);
 }
 
 // Participation-scheme rows that fit one tile (W <= 64K), in batches of RB rows. A wave
 // owns `seg` (<= 64) work items; lane i < seg first locates item i (its cluster, the
 // byte of its row and its size), then batches of RB rows are decoded with part_batch
 // while they share a cluster (always, under one global Mask), else row by row.
-template <int K, int MAXR, int RB, int SRC>
+template <int K, int MAXR, int RB, int SRC, bool PRE>
 __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint32_t *__restrict__ pay32,
                                                           uint64_t pay_base, const int64_t *__restrict__ ids,
                                                           const uint32_t *__restrict__ sg,
@@ -735,6 +744,16 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
         byte_l = o0 - pay_base;
         size_l = s.index[r + 1] - o0;
     }
+    // few chunks: each lane fetches its own row's participation dwords now, in one round
+    // trip for the whole segment
+    uint32_t pdw[kPreDwords] = {};
+    if constexpr (PRE) {
+        const uint32_t *__restrict__ p = pay32 + (byte_l >> 2);
+        const uint32_t b0 = ((uint32_t)byte_l & 3u) * 8u;
+        const uint32_t q0 = p[0], q1 = p[1], q2 = p[2];
+        pdw[0] = __builtin_amdgcn_alignbit(q1, q0, b0);
+        pdw[1] = __builtin_amdgcn_alignbit(q2, q1, b0);
+    }
     const uint64_t bad = __ballot(l < cnt && !valid);
     uint32_t *__restrict__ out_seg = out + i0 * W;
     if (bad) {
@@ -753,11 +772,17 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
         uint64_t rbyte[RB];
         bool raw[RB], ok[RB];
         uint32_t *orow[RB];
+        uint32_t pds[RB][kPreDwords];
         const uint64_t g0 = rd64(g_l, i);
         bool same = true;
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
             const uint32_t iu = min(i + u, cnt - 1);
+            if constexpr (PRE) {
+#pragma unroll
+                for (int k = 0; k < kPreDwords; ++k)
+                    pds[u][k] = (uint32_t)__builtin_amdgcn_readlane((int)pdw[k], (int)iu);
+            }
             rbyte[u] = rd64(byte_l, iu);
             raw[u] = rd64(size_l, iu) == 4ull * W;
             ok[u] = i + u < cnt && !((bad >> iu) & 1ull);
@@ -769,7 +794,7 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
                 tile_setup(t, s.meta + g0 * 2ull * W, W, 0, 0);
                 cached_g = g0;
             }
-            part_batch_any<RB>(t, pay32, rbyte, raw, ok, orow, m, C, W);
+            part_batch_any<RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds);
         } else {
 #pragma unroll
             for (int u = 0; u < RB; ++u) {
@@ -797,15 +822,21 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         const uint32_t seg = RB * nb;
         const uint64_t waves = (n + seg - 1) / seg;
         const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
-        if (ids)
-            hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds>), grid, block, 0, stream, s, p, pay_base, ids,
-                               sg, soff, first, n, o, seg, err);
-        else if (sg)
-            hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcStaged>), grid, block, 0, stream, s, p, pay_base,
-                               ids, sg, soff, first, n, o, seg, err);
-        else
-            hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcRange>), grid, block, 0, stream, s, p, pay_base,
-                               ids, sg, soff, first, n, o, seg, err);
+        const bool pre = (s.W - 1) / s.part_m < 32u * kPreDwords;    // at most 64 chunks
+        auto go = [&](auto pre_tag) {
+            constexpr bool P = decltype(pre_tag)::value;
+            if (ids)
+                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds, P>), grid, block, 0, stream, s, p, pay_base,
+                                   ids, sg, soff, first, n, o, seg, err);
+            else if (sg)
+                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcStaged, P>), grid, block, 0, stream, s, p,
+                                   pay_base, ids, sg, soff, first, n, o, seg, err);
+            else
+                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcRange, P>), grid, block, 0, stream, s, p,
+                                   pay_base, ids, sg, soff, first, n, o, seg, err);
+        };
+        if (pre) go(std::true_type{});
+        else go(std::false_type{});
         return hipGetLastError();
     }
     // rows of several tiles: one row at a time per wave
