@@ -117,10 +117,16 @@ enum {
                                     moves the needed packed bytes over PCIe through
                                     rotating staging buffers on a side stream (the host
                                     packs the rows of a gather) */
-    IBP_OPEN_PAYLOAD_HOST_ZERO_COPY = 2 /* kept in library-owned pinned host memory and read
+    IBP_OPEN_PAYLOAD_HOST_ZERO_COPY = 2, /* kept in library-owned pinned host memory and read
                                     by the decode kernels themselves over PCIe
                                     (GPU-initiated transfers, Sec. 4.4): no host packing,
                                     no staging copies */
+    IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED = 3 /* as ZERO_COPY, but the pinned copy starts
+                                    every packed row on a 128-byte boundary (each row padded
+                                    to a multiple of 128 bytes), so reading a row over PCIe
+                                    touches ceil(rb/128) 128-byte lines instead of up to one
+                                    more (Sec. 4.4 aligned transfers, applied to the layout);
+                                    costs host memory; clustered-scheme streams only */
 };
 
 /*
@@ -216,7 +222,7 @@ ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t
  * in device memory (d_row_ids, n_ids int64 values), for a handle whose payload is in
  * device memory (IBP_OPEN_PAYLOAD_DEVICE: every input is resident in HBM and the call
  * only enqueues the gather kernel) or read in place from pinned host memory
- * (IBP_OPEN_PAYLOAD_HOST_ZERO_COPY). Ids cannot be checked on the host: a row
+ * (IBP_OPEN_PAYLOAD_HOST_ZERO_COPY or _ALIGNED). Ids cannot be checked on the host: a row
  * whose id is out of range is written as zeros and counted in a device-side error
  * counter that ibp_device_errors() reads.
  * Errors: IBP_EINVAL (null pointers with n_ids > 0, or a handle opened with

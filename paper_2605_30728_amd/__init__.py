@@ -23,6 +23,7 @@ STATUS_NAMES = {0: "IBP_OK", 1: "IBP_EINVAL", 2: "IBP_ERANGE", 3: "IBP_ENOMEM", 
 IBP_OPEN_PAYLOAD_DEVICE = 0
 IBP_OPEN_PAYLOAD_HOST = 1
 IBP_OPEN_PAYLOAD_HOST_ZERO_COPY = 2
+IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED = 3
 IBP_STREAM_PARTICIPATION = 1
 
 

@@ -19,6 +19,8 @@ struct DevStream {
     uint32_t W;              // 32-bit words per row
     uint32_t G;              // rows per group
     uint32_t part_m;         // participation scheme: words per chunk; 0 = clustered scheme
+    uint32_t row_align;      // clustered scheme: rows of a cluster start every
+                             // roundup(rb, row_align) bytes (0: every rb bytes, no padding)
 };
 
 uint64_t div_magic(uint32_t G);

@@ -260,11 +260,11 @@ __global__ __launch_bounds__(kBlock) void k_decompress(DevStream s, const uint32
     if (W <= (uint32_t)(kWave * K)) {
         Tile<K, MAXR> t;
         tile_setup(t, mg, W, 0, 0);
-        const uint64_t rb = (t.bits + 7u) >> 3;
+        const uint64_t rb = row_stride((t.bits + 7u) >> 3, s.row_align);
         const SliceAt at{base + (r_lo - gstart) * rb, rb, out + (r_lo - first) * W, W};
         decode_rows(t, pay32, rows, at, W, 0);
     } else {
-        const uint64_t rb = (row_bits(mg, W) + 7u) >> 3;
+        const uint64_t rb = row_stride((row_bits(mg, W) + 7u) >> 3, s.row_align);
         const SliceAt at{base + (r_lo - gstart) * rb, rb, out + (r_lo - first) * W, W};
         decode_rows_tiled<K, MAXR>(mg, pay32, rows, at, W);
     }
@@ -329,11 +329,11 @@ __global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint
         if (W <= (uint32_t)(kWave * K)) {
             Tile<K, MAXR> t;
             tile_setup(t, mg, W, 0, 0);
-            at.rb = (t.bits + 7u) >> 3;
+            at.rb = row_stride((t.bits + 7u) >> 3, s.row_align);
             if constexpr (!STAGED) at.base = s.index[g];
             decode_rows(t, pay32, end - i, at, W, 0);
         } else {
-            at.rb = (row_bits(mg, W) + 7u) >> 3;
+            at.rb = row_stride((row_bits(mg, W) + 7u) >> 3, s.row_align);
             if constexpr (!STAGED) at.base = s.index[g];
             decode_rows_tiled<K, MAXR>(mg, pay32, end - i, at, W);
         }
@@ -442,7 +442,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
                 const uint32_t max_runs = wave_max(runs);
                 nh[u] = max_runs ? max_runs - 1u : 0u;
             }
-            const uint64_t rb = (tot[u] + 7u) >> 3;
+            const uint64_t rb = row_stride((tot[u] + 7u) >> 3, s.row_align);
             uint64_t rbyte;
             if constexpr (STAGED) rbyte = (uint32_t)__builtin_amdgcn_readlane((int)so, (int)i);
             else {

@@ -7,7 +7,9 @@
 //                                       scheme: (n_rows + 1) u64, of every row)
 //   d_payload payload_bytes + slack     packed rows (IBP_OPEN_PAYLOAD_DEVICE only; with
 //                                       IBP_OPEN_PAYLOAD_HOST_ZERO_COPY the kernels read
-//                                       the pinned host copy through its device address)
+//                                       the pinned host copy through its device address;
+//                                       with ..._ALIGNED that copy holds every row on a
+//                                       128-byte boundary and d_index its offsets)
 // The kernels read a word's 64-bit window as two dwords at its bit offset, so every
 // payload buffer the kernels see (device payload or staging) has kSlack readable bytes
 // past its last packed byte.
@@ -43,6 +45,7 @@ constexpr uint64_t kSlack = 256;                 // readable bytes past any payl
 constexpr uint64_t kStageBytes = 64ull << 20;    // one staging buffer
 constexpr int kStages = 3;                        // staging buffers in rotation
 constexpr int kIdSlots = 2;                       // host-id buffers in rotation
+constexpr uint64_t kRowAlign = 128;               // PCIe line: row start of aligned zero-copy
 constexpr uint64_t kCountBytes = dev::kCountLines * dev::kCountStride * 8;   // cache counters
 constexpr uint64_t kBlk = 256;                    // rows per host packing task (a chunk
                                                   // holds tens of them, for 16 threads)
@@ -246,6 +249,41 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
     return IBP_OK;
 }
 
+// Zero-copy payload with aligned rows: in the pinned copy every packed row of cluster g
+// starts on a kRowAlign boundary (row stride roundup(rb_g, kRowAlign), zero padding), and
+// the device index is replaced by the offsets of this layout. A GPU read of a row then
+// touches ceil(rb_g / 128) PCIe lines; a row at an arbitrary byte offset touches up to one
+// more.
+ibp_status setup_aligned_host_payload(ibp_handle *h, const StreamView &v) {
+    const ibp_desc &d = h->d;
+    const uint64_t ng = d.n_groups;
+    std::vector<uint64_t> aoff(ng + 1), rbs(ng);
+    aoff[0] = 0;
+    for (uint64_t g = 0; g < ng; ++g) {
+        const uint64_t n = v.rows_in_group(g);
+        rbs[g] = (v.off(g + 1) - v.off(g)) / n;
+        aoff[g + 1] = aoff[g] + n * ((rbs[g] + kRowAlign - 1) / kRowAlign * kRowAlign);
+    }
+    if (hipHostMalloc((void **)&h->h_payload, aoff[ng] + kSlack, hipHostMallocDefault) != hipSuccess)
+        return fail(IBP_ENOMEM, "pinned allocation for the aligned payload failed");
+    const uint8_t *src = v.payload();
+    uint8_t *dst = h->h_payload;
+    h->pool->run(ng, 256, [&](uint64_t lo, uint64_t hi) {
+        for (uint64_t g = lo; g < hi; ++g) {
+            const uint64_t n = v.rows_in_group(g), rb = rbs[g];
+            const uint64_t stride = (rb + kRowAlign - 1) / kRowAlign * kRowAlign;
+            for (uint64_t r = 0; r < n; ++r) {
+                uint8_t *o = dst + aoff[g] + r * stride;
+                std::memcpy(o, src + v.off(g) + r * rb, rb);
+                std::memset(o + rb, 0, stride - rb);
+            }
+        }
+    });
+    std::memset(dst + aoff[ng], 0, kSlack);
+    IBP_HIP(h, hipMemcpy(h->d_index, aoff.data(), 8 * (ng + 1), hipMemcpyHostToDevice));
+    return IBP_OK;
+}
+
 // Claim staging buffer b for a new chunk: the previous copy out of its pinned half must
 // have finished (host wait), and the next copy into its device half must wait for the
 // kernel that last read it (device wait on the copy stream).
@@ -376,12 +414,14 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     if (!out) return fail(IBP_EINVAL, "handle output is null");
     *out = nullptr;
     if (flags != IBP_OPEN_PAYLOAD_DEVICE && flags != IBP_OPEN_PAYLOAD_HOST &&
-        flags != IBP_OPEN_PAYLOAD_HOST_ZERO_COPY)
+        flags != IBP_OPEN_PAYLOAD_HOST_ZERO_COPY && flags != IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED)
         return fail(IBP_EINVAL, "unknown open flags");
     StreamView v;
     ibp_status st = parse_stream(stream, stream_bytes, v);
     if (st != IBP_OK) return st;
     const ibp_desc &d = v.d;
+    if (flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED && d.flags != 0)
+        return fail(IBP_EINVAL, "aligned rows need a clustered-scheme stream (flags = 0)");
     if (d.group_rows > 1 && d.n_rows > ~0ull / d.group_rows)
         return fail(IBP_EINVAL, "n_rows * group_rows must stay below 2^64");
     if (2ull * d.row_bytes * 8 > 0xFFFFFFFFull) return fail(IBP_EINVAL, "row_bytes too large");
@@ -427,9 +467,10 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
             return bail(fail(IBP_EHIP, "payload upload failed"));
         h->k_payload = h->d_payload;
     } else {
-        st = setup_host_path(h, v);
+        st = flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED ? setup_aligned_host_payload(h, v)
+                                                             : setup_host_path(h, v);
         if (st != IBP_OK) return bail(st);
-        if (flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) {
+        if (flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY || flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED) {
             void *dp = nullptr;
             if (hipHostGetDevicePointer(&dp, h->h_payload, 0) != hipSuccess || !dp)
                 return bail(fail(IBP_EHIP, "pinned payload is not mapped for the device"));
@@ -446,6 +487,7 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     h->ds.n_groups = d.n_groups;
     h->ds.g_magic = dev::div_magic(d.group_rows);
     h->ds.part_m = (d.flags & IBP_STREAM_PARTICIPATION) ? d.chunk_bytes / 4 : 0;
+    h->ds.row_align = flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED ? (uint32_t)kRowAlign : 0;
     h->ds.W = d.row_bytes / 4;
     h->ds.G = d.group_rows;
     ignore(hipSetDevice(prev));

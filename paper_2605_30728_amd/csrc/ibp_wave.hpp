@@ -33,6 +33,12 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(v), 63);
 }
 
+// Distance between consecutive packed rows of a cluster: the packed size, or the packed
+// size rounded up to `align` bytes (a power of two) when rows start on aligned slots.
+__device__ __forceinline__ uint64_t row_stride(uint64_t rb, uint32_t align) {
+    return align ? (rb + align - 1) & ~(uint64_t)(align - 1) : rb;
+}
+
 __device__ __forceinline__ uint64_t wave_slot() {
     return (uint64_t)blockIdx.x * kWavesPerBlock +
            (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));

@@ -17,7 +17,8 @@ from workloads import CONFIGS, gen_all_rows, gen_rows, gnn_batch_ids, structured
 pytestmark = pytest.mark.gpu
 
 FLAGS = {"device": ibp.IBP_OPEN_PAYLOAD_DEVICE, "host": ibp.IBP_OPEN_PAYLOAD_HOST,
-         "zero_copy": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY}
+         "zero_copy": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY,
+         "zero_copy_aligned": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED}
 
 
 def say(*a):
@@ -73,7 +74,7 @@ SMALL = [("floats", 300, 400, 32), ("random", 97, 12, 5), ("specials", 70, 16, 7
          ("alternating", 45, 520, 9), ("floats", 40, 4096, 32), ("random", 19, 4096, 8)]
 
 
-@pytest.mark.parametrize("flags", ["device", "host", "zero_copy"])
+@pytest.mark.parametrize("flags", ["device", "host", "zero_copy", "zero_copy_aligned"])
 @pytest.mark.parametrize("kind,n,L,G", SMALL, ids=[f"{c[0]}-{c[1]}x{c[2]}-G{c[3]}" for c in SMALL])
 def test_decompress_small(torch, kind, n, L, G, flags):
     rows = structured_rows(kind, n, L, seed=n + 3 * L)
@@ -90,7 +91,8 @@ def test_decompress_small(torch, kind, n, L, G, flags):
 
 
 @pytest.mark.parametrize("mode", ["device_payload_host_ids", "device_payload_device_ids", "host_payload",
-                                  "zero_copy_host_ids", "zero_copy_device_ids"])
+                                  "zero_copy_host_ids", "zero_copy_device_ids", "zero_copy_aligned_host_ids",
+                                  "zero_copy_aligned_device_ids"])
 @pytest.mark.parametrize("kind,n,L,G", SMALL, ids=[f"{c[0]}-{c[1]}x{c[2]}-G{c[3]}" for c in SMALL])
 def test_gather_small(torch, kind, n, L, G, mode):
     rows = structured_rows(kind, n, L, seed=n + 3 * L)
@@ -101,6 +103,7 @@ def test_gather_small(torch, kind, n, L, G, mode):
     want = oracle.decode_rows(stream, ids, L)
     say(f"[gather] {kind} n={n} L={L} G={G} mode={mode} n_ids={ids.size}")
     flags = (ibp.IBP_OPEN_PAYLOAD_HOST if mode == "host_payload" else
+             ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED if mode.startswith("zero_copy_aligned") else
              ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero_copy") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
     got, errs = gpu_gather(torch, stream, ids, L, flags, device_ids=mode.endswith("device_ids"))
     assert errs == 0
@@ -248,9 +251,10 @@ def test_gnn_gather_full(torch):
     ids = gnn_batch_ids(cfg.n_rows, cfg.extra["seeds"], cfg.extra["fanouts"], batch_index=0)
     sample = np.random.default_rng(5).choice(ids.size, 3000, replace=False)
     want_sample = oracle.decode_rows(stream, ids[sample], cfg.row_bytes)
-    for mode in ("device_ids", "host_ids", "host_payload", "zero_copy_device_ids"):
+    for mode in ("device_ids", "host_ids", "host_payload", "zero_copy_device_ids", "zero_copy_aligned_device_ids"):
         say(f"[gnn gather] mode={mode} n_ids={ids.size}")
         flags = (ibp.IBP_OPEN_PAYLOAD_HOST if mode == "host_payload" else
+                 ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED if mode.startswith("zero_copy_aligned") else
                  ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero_copy") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
         got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=mode.endswith("device_ids"))
         assert errs == 0
@@ -288,9 +292,10 @@ def test_dlrm_full(torch):
     want = rows[ids]
     sample = np.random.default_rng(9).choice(ids.size, 2000, replace=False)
     assert np.array_equal(oracle.decode_rows(stream, ids[sample], cfg.row_bytes), want[sample])
-    for mode in ("device_ids", "zero_copy_device_ids"):
+    for mode in ("device_ids", "zero_copy_device_ids", "zero_copy_aligned_device_ids"):
         say(f"[dlrm] gather mode={mode} n_ids={ids.size}")
-        flags = ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE
+        flags = (ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED if mode.startswith("zero_copy_aligned") else
+                 ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
         got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=True)
         assert errs == 0
         assert np.array_equal(got, want)       # [2048, 26, 128] fp32, sample-major
@@ -350,7 +355,7 @@ def test_independent_handles_on_threads(torch):
     stream = oracle.compress(rows, 32)
     rng = np.random.default_rng(5)
     jobs = [(flags, rng.integers(0, 4000, size=3000).astype(np.int64))
-            for flags in (FLAGS["device"], FLAGS["host"], FLAGS["zero_copy"], FLAGS["device"])]
+            for flags in (FLAGS["device"], FLAGS["host"], FLAGS["zero_copy"], FLAGS["zero_copy_aligned"])]
     wants = [oracle.decode_rows(stream, ids, 256) for _, ids in jobs]
     results, errors = [None] * len(jobs), []
     say("[threads] 4 handles on 4 threads")
@@ -378,3 +383,16 @@ def test_independent_handles_on_threads(torch):
     for k in range(len(jobs)):
         assert np.array_equal(results[k][0], wants[k])
         assert np.array_equal(results[k][1], rows)
+
+
+
+def test_aligned_zero_copy_rejects_participation_streams(torch):
+    rows = structured_rows("floats", 100, 64, seed=8)
+    ps = oracle.compress(rows, 100, chunk_bytes=8, threshold=(4, 5))
+    with pytest.raises(ibp.IbpError) as e:
+        ibp.ibp_open(ps, 0, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED)
+    assert e.value.status == ibp.IBP_EINVAL
+    with ibp.ibp_open(oracle.compress(rows, 16), 0, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED) as h:
+        with pytest.raises(ibp.IbpError) as e:
+            ibp.ibp_cache_create(h, np.arange(10))
+        assert e.value.status == ibp.IBP_EINVAL
