@@ -544,7 +544,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-e2e", action="store_true")
-    ap.add_argument("--e2e-steps", type=int, default=20)
+    ap.add_argument("--e2e-steps", type=int, default=40)
     ap.add_argument("--scheme", default="clustered", choices=["clustered", "participation"],
                     help="clustered: Mask/Bitval per cluster of the workload's G rows with T = G (the default); "
                          "participation: the thresholded scheme with participation bits")
