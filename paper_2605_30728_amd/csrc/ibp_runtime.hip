@@ -236,6 +236,10 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
     }
     if (h->flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) return IBP_OK;   // no staging: kernels read in place
     if (d.n_groups > 0xFFFFFFFFull) return fail(IBP_EINVAL, "too many clusters for the PCIe path");
+    // a staged chunk holds at least one whole row with its tables (gathers) or one packed
+    // row (ranges), so every call can make progress without overrunning a stage
+    if ((uint64_t)d.row_bytes + 72 > kStageBytes)
+        return fail(IBP_EINVAL, "rows larger than a staging buffer need another placement");
     for (int b = 0; b < kStages; ++b) {
         if (hipHostMalloc((void **)&h->h_stage[b], kStageBytes + kSlack, hipHostMallocDefault) != hipSuccess)
             return fail(IBP_ENOMEM, "pinned allocation for staging failed");

@@ -396,3 +396,22 @@ def test_aligned_zero_copy_rejects_participation_streams(torch):
         with pytest.raises(ibp.IbpError) as e:
             ibp.ibp_cache_create(h, np.arange(10))
         assert e.value.status == ibp.IBP_EINVAL
+
+
+
+def test_host_placement_rejects_rows_larger_than_a_stage(torch):
+    """A row that cannot fit one 64 MiB staging buffer is refused at open for the staged
+    placement (and accepted by the others)."""
+    L = 64 << 20
+    rows = np.zeros((1, L), np.uint8)
+    rows[0, ::4097] = 7
+    stream = ibp.ibp_compress(rows, 1)
+    say("[edge] 64 MiB row on the staged placement")
+    with pytest.raises(ibp.IbpError) as e:
+        ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_HOST)
+    assert e.value.status == ibp.IBP_EINVAL
+    with ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_DEVICE) as h:
+        out = torch.empty(L, dtype=torch.uint8, device="cuda")
+        ibp.ibp_decompress(h, 0, 1, out)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), rows[0])
