@@ -299,6 +299,22 @@ def test_dlrm_full(torch):
         got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=True)
         assert errs == 0
         assert np.array_equal(got, want)       # [2048, 26, 128] fp32, sample-major
+    # the compressed device cache over the full tables: the 2M most popular rows cached,
+    # hits decoded from HBM and misses from pinned host memory in one kernel
+    from workloads import dlrm_hot_order
+    hot = dlrm_hot_order(x["tables"], x["rows_per_table"], n=2_000_000)
+    say(f"[dlrm] cache of {hot.size} rows, n_ids={ids.size}")
+    with ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) as h:
+        with ibp.ibp_cache_create(h, hot) as c:
+            d_ids = torch.from_numpy(ids).cuda()
+            out = torch.empty(ids.size * cfg.row_bytes, dtype=torch.uint8, device="cuda")
+            ibp.ibp_cache_gather(c, d_ids, out)
+            torch.cuda.synchronize()
+            assert np.array_equal(out.cpu().numpy().reshape(-1, cfg.row_bytes), want)
+            st = ibp.ibp_cache_get_stats(c)
+            hits = int(np.isin(ids, hot).sum())
+            assert st["hits"] == hits and st["misses"] == ids.size - hits and hits > ids.size // 2
+        assert ibp.ibp_device_errors(h) == 0
     del rows, stream
     gc.collect()
 
@@ -314,9 +330,10 @@ def test_big_gnn_full(torch):
     want = rows[ids]
     sample = np.random.default_rng(10).choice(ids.size, 2000, replace=False)
     assert np.array_equal(oracle.decode_rows(stream, ids[sample], cfg.row_bytes), want[sample])
-    for mode in ("device_ids", "zero_copy_device_ids"):
+    for mode in ("device_ids", "zero_copy_device_ids", "zero_copy_aligned_device_ids"):
         say(f"[big_gnn] gather mode={mode} n_ids={ids.size}")
-        flags = ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE
+        flags = (ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED if mode.startswith("zero_copy_aligned") else
+                 ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
         got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=True)
         assert errs == 0
         assert np.array_equal(got, want)

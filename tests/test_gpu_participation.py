@@ -142,3 +142,29 @@ def test_participation_gnn_gather_full(torch):
             ibp.ibp_gather_decompress(h, ids, out, out_cap=ids.size * cfg.row_bytes)
             torch.cuda.synchronize()
             assert np.array_equal(_rows(out, ids.size, cfg.row_bytes), want)
+
+
+
+@pytest.mark.timeout(600)
+def test_participation_kv_full(torch):
+    """All 32 layers of the bf16 KV workload (4 GiB raw) under one global Mask at T = 0.8n
+    with 8-byte chunks, streamed layer by layer through every placement; layers checked
+    against the original rows, sampled rows against the oracle."""
+    import gc
+    cfg = CONFIGS["kv_bf16"]
+    rows = gen_all_rows(cfg)
+    s = ibp.ibp_compress_ex(rows, cfg.n_rows, 8, (4, 5), 1)
+    n = cfg.extra["rows_per_layer"]
+    sample = np.random.default_rng(4).choice(cfg.n_rows, 1500, replace=False)
+    assert np.array_equal(oracle.decode_rows(s, sample, cfg.row_bytes), rows[sample])
+    for flags in (ibp.IBP_OPEN_PAYLOAD_DEVICE, ibp.IBP_OPEN_PAYLOAD_HOST, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY):
+        say(f"[part kv full] flags={flags}")
+        with ibp.ibp_open(s, 0, flags) as h:
+            out = torch.empty(n * cfg.row_bytes, dtype=torch.uint8, device="cuda")
+            for layer in range(cfg.extra["layers"]):
+                ibp.ibp_decompress(h, layer * n, n, out)
+                torch.cuda.synchronize()
+                got = out.cpu().numpy().reshape(n, cfg.row_bytes)
+                assert np.array_equal(got, rows[layer * n:(layer + 1) * n]), (flags, layer)
+    del rows, s
+    gc.collect()
