@@ -402,9 +402,15 @@ def micro(args):
         torch.cuda.synchronize()
         return float(np.median([ev[k].elapsed_time(ev[k + 1]) for k in range(iters)])) * 1e-3
 
+    part = args.scheme == "participation"
+    num, den = (int(x) for x in args.threshold.split("/"))
+
     def point(L, target, out):
         rows = micro_rows(n, L, target)
-        stream = ibp.ibp_compress(rows, G)
+        if part:   # one global Mask, participation bits per chunk (the paper's own scheme)
+            stream = ibp.ibp_compress_ex(rows, n, args.chunk_bytes, (num, den), args.sample_every)
+        else:
+            stream = ibp.ibp_compress(rows, G)
         d = ibp.ibp_describe(stream)
         pay = max(d["payload_bytes"], 1)
         ref = torch.from_numpy(rows.reshape(-1)).cuda()
@@ -447,7 +453,10 @@ def micro(args):
         del out
     print(json.dumps({"metric": "decompression throughput relative to the no-decode mock system",
                       "unit": "fraction of mock", "n_gpus": 1, "tensors": n, "iterations": iters,
-                      "group_rows": G, "raw_h2d_GBps_1GiB": round(raw, 2), "data": "synthetic",
+                      "scheme": ({"name": "participation", "chunk_bytes": args.chunk_bytes,
+                                  "threshold": args.threshold, "mask_rows": n} if part else
+                                 {"name": "clustered", "group_rows": G}),
+                      "raw_h2d_GBps_1GiB": round(raw, 2), "data": "synthetic",
                       "points": points}), flush=True)
 
 
