@@ -54,7 +54,17 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decompressed GB/s (HBM roofline %) + effective H2D GB/s vs raw PCIe"
 HBM_PEAK_GBS = 8000.0
-KERNEL_SRC = os.path.join(ROOT, "paper_2605_30728_amd", "csrc", "ibp_kernels.hip")
+# the sources the profiled kernels are compiled from (a profile's counters stand only
+# while these hash to the value recorded with them)
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2605_30728_amd", "csrc", f)
+                  for f in ("ibp_kernels.hip", "ibp_cache_kernels.hip", "ibp_wave.hpp", "ibp_device.hpp")]
+
+
+def kernel_sources_sha256():
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
 GATHERS = ("gnn_gather", "dlrm", "big_gnn")
 STREAMS = ("kv_bf16", "tiny_gnn")
 DESCRIPTIONS = {
@@ -101,7 +111,7 @@ def measured_traffic(workload, part=False):
     m_bytes = re.search(r"traffic_bytes_per_launch:\s*(\d+)", text)
     if not m_hash or not m_bytes:
         return None
-    if hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest() != m_hash.group(1):
+    if kernel_sources_sha256() != m_hash.group(1):
         return None
     return int(m_bytes.group(1))
 
@@ -200,7 +210,9 @@ class Layout:
 
     def gather_alg(self, ids):
         """ids, packed rows read, rows written, and per touched cluster its Mask/Bitval
-        (plus its index entry; per row two index entries in the participation scheme)."""
+        (plus its index entry; per row two index entries in the participation scheme).
+        The Mask/Bitval count is the format's 2 * row_bytes even where the kernels read a
+        cluster's compact slot instead (fewer bytes)."""
         clusters = np.unique(ids // self.G).size
         idx = 16 * ids.size if self.part else 8 * clusters
         return int(ids.size * 8 + self.sizes(ids).sum() + ids.size * self.L + clusters * 2 * self.L + idx)
@@ -613,9 +625,10 @@ def main():
     log(f"[bench] compressed in {compress_s:.2f}s ({threads} threads): payload {d['payload_bytes'] / 1e6:.1f} MB, "
         f"stream {d['stream_bytes'] / 1e6:.1f} MB, raw {cfg.n_rows * L / 1e6:.1f} MB")
 
+    h = ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_DEVICE)
+    gather_meta = ibp.ibp_get_stats(h)["gather_meta_bytes"]
     steps = Steps(wl, cfg, Wm + K, layout)
     out = torch.empty(max(steps.rows) * L, dtype=torch.uint8, device="cuda")
-    h = ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_DEVICE)
     if wl in GATHERS:
         d_units = [torch.from_numpy(u).cuda() for u in steps.units]
 
@@ -715,7 +728,8 @@ def main():
                      "kernel": kernel_name(wl, W, part), "kernel_us": round(kern_ms * 1e3, 2),
                      "kernel_us_bracketed_median": round(float(np.median(kern_all)) * 1e3, 2),
                      "kernel_us_bracketed_min": round(float(kern_all.min()) * 1e3, 2),
-                     "algorithmic_bytes_per_launch": int(alg_avg), "d2d_copy_GBps": round(copy_gbs, 1)},
+                     "algorithmic_bytes_per_launch": int(alg_avg), "d2d_copy_GBps": round(copy_gbs, 1),
+                     "gather_meta_bytes_per_cluster": gather_meta if wl in GATHERS else None},
         "uncompressed_device": {"GBps": round(out_bytes / wall_u / 1e9, 2),
                                 "speedup_of_compressed": round(wall_u / wall, 3)},
         "cpu_baseline": cpu,

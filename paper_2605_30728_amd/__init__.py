@@ -54,7 +54,8 @@ class ibp_params(ctypes.Structure):
 class ibp_stats(ctypes.Structure):
     _fields_ = [("calls", ctypes.c_uint64), ("rows_out", ctypes.c_uint64),
                 ("out_bytes", ctypes.c_uint64), ("h2d_bytes", ctypes.c_uint64),
-                ("h2d_payload_bytes", ctypes.c_uint64), ("host_pack_ns", ctypes.c_uint64)]
+                ("h2d_payload_bytes", ctypes.c_uint64), ("host_pack_ns", ctypes.c_uint64),
+                ("gather_meta_bytes", ctypes.c_uint64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

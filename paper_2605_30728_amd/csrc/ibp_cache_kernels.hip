@@ -9,6 +9,8 @@
 // decoded on its own (its cluster's Mask/Bitval, a scan of popcount(~Mask), the holes
 // deposit), all loads of the batch issued before any word is rebuilt. The only change is
 // that a row's packed bytes are located by an absolute address chosen per request.
+#include <type_traits>
+
 #include "ibp_device.hpp"
 #include "ibp_wave.hpp"
 
@@ -22,7 +24,7 @@ struct Slot {
     uint64_t val;   // cache entry
 };
 
-template <int K, int RB>
+template <int K, int RB, int FORM>
 __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView c, const int64_t *__restrict__ ids,
                                                           uint64_t n, uint32_t *__restrict__ out,
                                                           unsigned long long *err) {
@@ -60,7 +62,8 @@ __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView 
     // byte address of the row's packed bits: the slab entry for a hit; for a miss the
     // cluster's payload offset, to which the row's index times its packed size is added
     // once the size is known from the Mask
-    const uint64_t base_l = hit ? (uint64_t)c.slab + (val & 0xFFFFFFFFFFull) : (uint64_t)c.host_payload + s.index[g_l];
+    const uint64_t off_l = hit ? (val & 0xFFFFFFFFFFull) : s.index[g_l];
+    const uint32_t mul_l = hit ? 0u : r_l;
     const uint64_t nhit = __ballot(valid && hit), nmiss = __ballot(valid && !hit);
     const uint64_t bad = __ballot(l < cnt && !valid);
     if (l == 0) {
@@ -82,20 +85,25 @@ __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView 
                (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, (int)i);
     };
     auto slot_of = [&](uint32_t i) { return i < cnt ? i : cnt - 1; };
-    RowMeta<K> meta[RB];
+    RowMeta<K, FORM> meta[RB];
 #pragma unroll
-    for (int u = 0; u < RB; ++u)
-        load_row_meta<K>(meta[u], s.meta + rd64(g_l, slot_of(u)) * 2ull * W, W);
+    for (int u = 0; u < RB; ++u) {
+        const uint64_t g = rd64(g_l, slot_of(u));
+        load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * meta_slot_bytes<K>(), W);
+    }
+#pragma unroll
+    for (int u = 0; u < RB; ++u) hold_row_meta(meta[u]);
     uint32_t nm[RB][K], bv[RB][K], ofs[RB][K], d0[RB][K], d1[RB][K], nh[RB], bit0[RB];
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
         const uint32_t i = slot_of(u);
-        uint32_t cntw[K], runs = 0;
+        uint32_t cntw[K], runs = 0, mw[K], bw[K];
+        expand_row_meta(meta[u], mw, bw);
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const bool in_row = l + kWave * j < W;
-            nm[u][j] = in_row ? ~meta[u].m[j] : 0u;
-            bv[u][j] = in_row ? meta[u].b[j] : 0u;
+            nm[u][j] = in_row ? ~mw[j] : 0u;
+            bv[u][j] = in_row ? bw[j] : 0u;
             cntw[j] = (uint32_t)__builtin_popcount(nm[u][j]);
             runs = max(runs, run_count(nm[u][j]));
         }
@@ -103,10 +111,11 @@ __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView 
         const uint32_t max_runs = wave_max(runs);
         nh[u] = max_runs ? max_runs - 1u : 0u;
         const uint64_t rb = (tot + 7u) >> 3;
-        const bool hit_i = (nhit >> i) & 1ull;
-        const uint64_t addr = rd64(base_l, i) +
-                              (hit_i ? 0ull : (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)r_l, (int)i) * rb);
-        const uint32_t *__restrict__ p = reinterpret_cast<const uint32_t *>(addr & ~3ull);
+        // a select of the two buffers, not an integer address, keeps the loads global
+        // (not flat) and the choice free of branches
+        const uint8_t *__restrict__ buf = ((nhit >> i) & 1ull) ? c.slab : c.host_payload;
+        const uint64_t addr = rd64(off_l, i) + (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)mul_l, (int)i) * rb;
+        const uint32_t *__restrict__ p = reinterpret_cast<const uint32_t *>(buf + (addr & ~3ull));
         bit0[u] = ((uint32_t)addr & 3u) * 8u;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
@@ -137,16 +146,16 @@ hipError_t launch_cache_gather(const DevStream &s, const CacheView &c, const int
     if (n == 0) return hipSuccess;
     auto *o = static_cast<uint32_t *>(out);
     auto grid = [&](uint64_t rb) { return dim3((unsigned)(((n + rb - 1) / rb + kWavesPerBlock - 1) / kWavesPerBlock)); };
-    if (s.W <= 64)
-        hipLaunchKernelGGL((k_cache_gather<1, 8>), grid(8), dim3(kBlock), 0, stream, s, c, ids, n, o, err);
-    else if (s.W <= 128)
-        hipLaunchKernelGGL((k_cache_gather<2, 4>), grid(4), dim3(kBlock), 0, stream, s, c, ids, n, o, err);
-    else if (s.W <= 256)
-        hipLaunchKernelGGL((k_cache_gather<4, 2>), grid(2), dim3(kBlock), 0, stream, s, c, ids, n, o, err);
-    else if (s.W <= 512)
-        hipLaunchKernelGGL((k_cache_gather<8, 1>), grid(1), dim3(kBlock), 0, stream, s, c, ids, n, o, err);
-    else
-        return hipErrorInvalidValue;
+    auto go = [&](auto kk, auto rb) {
+        constexpr int KK = decltype(kk)::value, R = decltype(rb)::value;
+        if (s.slots) hipLaunchKernelGGL((k_cache_gather<KK, R, kMetaSlots>), grid(R), dim3(kBlock), 0, stream, s, c, ids, n, o, err);
+        else hipLaunchKernelGGL((k_cache_gather<KK, R, kMetaRaw>), grid(R), dim3(kBlock), 0, stream, s, c, ids, n, o, err);
+    };
+    if (s.W <= 64) go(std::integral_constant<int, 1>{}, std::integral_constant<int, 8>{});
+    else if (s.W <= 128) go(std::integral_constant<int, 2>{}, std::integral_constant<int, 4>{});
+    else if (s.W <= 256) go(std::integral_constant<int, 4>{}, std::integral_constant<int, 2>{});
+    else if (s.W <= 512) go(std::integral_constant<int, 8>{}, std::integral_constant<int, 1>{});
+    else return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

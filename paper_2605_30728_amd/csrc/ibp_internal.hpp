@@ -5,6 +5,7 @@
 #include <cstdint>
 #include <functional>
 #include <string>
+#include <vector>
 
 #include "ibp.h"
 
@@ -55,5 +56,14 @@ private:
     struct State;
     State *st_;
 };
+
+// Compact device metadata of the clustered scheme's row gathers (ibp_meta_dict.cpp): a
+// fixed-size slot per cluster (meta_slot_bytes(K) bytes, cluster g at g times that) with
+// up to kSlotPairs distinct (Mask, Bitval) pairs and a 4-bit pair index per word, laid out
+// for lanes owning K words each. Returns whether every cluster fits a slot.
+constexpr uint32_t kSlotPairs = 8;
+constexpr uint64_t meta_slot_bytes(uint32_t K) { return (8ull * kSlotPairs + 32ull * K + 127) / 128 * 128; }
+bool build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32_t K, Pool &pool,
+                      std::vector<uint8_t> &slots);
 
 }  // namespace ibp

@@ -351,7 +351,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint
 // issued after a batch's stores would wait for those stores as well). Rows are rebuilt
 // with the generic run walk: with a setup per row, precomputed runs would cost more than
 // they save.
-template <int K, int RB, bool STAGED>
+template <int K, int RB, bool STAGED, int FORM>
 __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint32_t *__restrict__ pay32,
                                                          const int64_t *__restrict__ ids,
                                                          const uint32_t *__restrict__ sg,
@@ -405,10 +405,14 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
     const uint32_t nb = (cnt + RB - 1) / RB;
     for (uint32_t bb = 0; bb < nb; ++bb) {
         const uint32_t base_i = bb * RB;
-        RowMeta<K> meta[RB];
+        RowMeta<K, FORM> meta[RB];
 #pragma unroll
-        for (int u = 0; u < RB; ++u)
-            load_row_meta<K>(meta[u], s.meta + rd64(g_lo, g_hi, slot_of(base_i + u)) * 2ull * W, W);
+        for (int u = 0; u < RB; ++u) {
+            const uint64_t g = rd64(g_lo, g_hi, slot_of(base_i + u));
+            load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * meta_slot_bytes<K>(), W);
+        }
+#pragma unroll
+        for (int u = 0; u < RB; ++u) hold_row_meta(meta[u]);
         // per row: variant positions, Bitval, bit offsets of the words inside the packed
         // row (without the row's byte misalignment bit0), hole iterations, packed bits
         uint32_t nm[RB][K], bv[RB][K], ofs[RB][K], d0[RB][K], d1[RB][K], nh[RB], tot[RB], bit0[RB];
@@ -429,12 +433,13 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
                 nh[u] = nh[up];
                 tot[u] = tot[up];
             } else {
-                uint32_t cntw[K], runs = 0;
+                uint32_t cntw[K], runs = 0, mw[K], bw[K];
+                expand_row_meta(meta[u], mw, bw);
 #pragma unroll
                 for (int j = 0; j < K; ++j) {
                     const bool in_row = l + kWave * j < W;
-                    nm[u][j] = in_row ? ~meta[u].m[j] : 0u;
-                    bv[u][j] = in_row ? meta[u].b[j] : 0u;
+                    nm[u][j] = in_row ? ~mw[j] : 0u;
+                    bv[u][j] = in_row ? bw[j] : 0u;
                     cntw[j] = (uint32_t)__builtin_popcount(nm[u][j]);
                     runs = max(runs, run_count(nm[u][j]));
                 }
@@ -855,13 +860,6 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
     return hipGetLastError();
 }
 
-// Words-per-lane tile shape for a row of W words: (K, MAXR).
-int pick_k(uint32_t W) {
-    if (W <= 64) return 1;
-    if (W <= 128) return 2;
-    if (W <= 256) return 4;
-    return 8;
-}
 
 }  // namespace
 
@@ -878,7 +876,7 @@ hipError_t launch_part(const DevStream &s, const uint8_t *payload, uint64_t pay_
                        unsigned long long *err, hipStream_t stream) {
     const auto *p = reinterpret_cast<const uint32_t *>(payload);
     auto *o = static_cast<uint32_t *>(out);
-    switch (pick_k(s.W)) {
+    switch (words_per_lane(s.W)) {
     case 1: return launch_part_k<1, 4>(s, p, pay_base, ids, sg, soff, first, n, o, err, stream);
     case 2: return launch_part_k<2, 4>(s, p, pay_base, ids, sg, soff, first, n, o, err, stream);
     case 4: return launch_part_k<4, 2>(s, p, pay_base, ids, sg, soff, first, n, o, err, stream);
@@ -894,7 +892,7 @@ hipError_t launch_decompress(const DevStream &s, const uint8_t *payload, uint64_
     // rows per wave: a whole cluster (at most 64 rows), halved while the launch would have
     // fewer than ~16k waves (2 per wave slot of the chip), down to one batch of rows;
     // every slice repeats its cluster's setup, which is small next to its rows
-    const int k = pick_k(s.W);
+    const int k = words_per_lane(s.W);
     const uint32_t min_rows = k == 1 ? 8 : (k == 2 ? 4 : (k == 4 ? 2 : 1));
     uint32_t rpu = s.G <= 64 ? s.G : 64;
     while (rpu > min_rows && (g1 - g0 + 1) * ((s.G + rpu - 1) / rpu) < 16384) rpu = (rpu + 1) / 2;
@@ -919,7 +917,7 @@ hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64
     if (s.part_m) return launch_part(s, payload, 0, ids, sg, soff, 0, n, out, err, stream);
     const auto *p = reinterpret_cast<const uint32_t *>(payload);
     auto *o = static_cast<uint32_t *>(out);
-    const int k = pick_k(s.W);
+    const int k = words_per_lane(s.W);
     if (s.W > 512) {
         const uint32_t seg = 16;
         const uint64_t blocks = ((n + seg - 1) / seg + kWavesPerBlock - 1) / kWavesPerBlock;
@@ -938,13 +936,17 @@ hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64
     const uint32_t seg = (uint32_t)rb_sel;
     const uint64_t blocks = ((n + seg - 1) / seg + kWavesPerBlock - 1) / kWavesPerBlock;
     dim3 grid((unsigned)blocks), block(kBlock);
-#define IBP_GATHER_ROWS(KK, RB)                                                                             \
-    do {                                                                                                    \
-        if (soff)                                                                                           \
-            hipLaunchKernelGGL((k_gather_rows<KK, RB, true>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err); \
-        else                                                                                                \
-            hipLaunchKernelGGL((k_gather_rows<KK, RB, false>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err); \
-    } while (0)
+    auto go = [&](auto kk, auto rb) {
+        constexpr int KK = decltype(kk)::value, R = decltype(rb)::value;
+        if (soff) {
+            if (s.slots) hipLaunchKernelGGL((k_gather_rows<KK, R, true, kMetaSlots>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err);
+            else hipLaunchKernelGGL((k_gather_rows<KK, R, true, kMetaRaw>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err);
+        } else {
+            if (s.slots) hipLaunchKernelGGL((k_gather_rows<KK, R, false, kMetaSlots>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err);
+            else hipLaunchKernelGGL((k_gather_rows<KK, R, false, kMetaRaw>), grid, block, 0, stream, s, p, ids, sg, soff, n, o, seg, err);
+        }
+    };
+#define IBP_GATHER_ROWS(KK, RB) go(std::integral_constant<int, KK>{}, std::integral_constant<int, RB>{})
     switch (k) {
     case 1: IBP_GATHER_ROWS(1, 8); break;
     case 2: IBP_GATHER_ROWS(2, 4); break;

@@ -1,0 +1,87 @@
+// Compact device form of the clustered scheme's Mask/Bitval words, read by the row
+// gathers (the kernel side is load_row_meta_slot / expand_row_meta in ibp_wave.hpp).
+//
+// A cluster stores one (Mask_w, Bitval_w) pair per 32-bit word w (Sec. 3.2). The words of
+// a row repeat few distinct pairs (columns of one feature table share their invariant
+// exponent and mantissa bits), and a gather reads a cluster's metadata for every row it
+// decodes. So every cluster also gets a fixed-size slot, at slot_bytes(K) * g of the
+// slot area, holding
+//
+//   pairs   kSlotPairs x {u32 Mask, u32 Bitval}: the cluster's distinct pairs in order of
+//           first appearance (unused entries zero)
+//   index   32*K bytes: a 4-bit pair index per word, laid out for the wave that decodes
+//           the row: lane l owns words l, l+64, ..., l+64*(K-1) and their K indices sit
+//           together in bits [4*K*l, 4*K*l + 4*K) of the area (index j in bits 4j..4j+3
+//           of that field), so a lane fetches all of its indices with one load
+//
+// Words past the row's end (lanes of the last tile) take index 0. A slot's address
+// follows from the cluster number alone, so its loads need nothing but the row id; at
+// K <= 2 a slot is one 128-byte line, against 8W bytes of raw metadata. The kernels read
+// slots only when every cluster of the stream fits one (a per-row choice of form would
+// cost every row a branch); otherwise the slots are dropped and the raw words are read.
+#include <atomic>
+#include <cstring>
+
+#include "ibp_internal.hpp"
+
+namespace ibp {
+
+namespace {
+
+inline uint32_t rd32(const uint8_t *p) {
+    uint32_t v;
+    std::memcpy(&v, p, 4);
+    return v;
+}
+
+}  // namespace
+
+bool build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32_t K, Pool &pool,
+                      std::vector<uint8_t> &slots) {
+    std::atomic<bool> all_fit{true};
+    const uint64_t S = meta_slot_bytes(K), raw = 8ull * W;
+    slots.assign(std::max<uint64_t>(n_groups * S, 8), 0);
+    pool.run(n_groups, 1024, [&](uint64_t lo, uint64_t hi) {
+        std::vector<uint8_t> word_pair(W);
+        for (uint64_t g = lo; g < hi; ++g) {
+            const uint8_t *mg = meta + g * raw;
+            uint8_t *slot = slots.data() + g * S;
+            uint32_t pm[kSlotPairs], pb[kSlotPairs], n = 0;
+            bool fits = true;
+            for (uint32_t w = 0; w < W && fits; ++w) {
+                const uint32_t m = rd32(mg + 4ull * w), b = rd32(mg + 4ull * (W + w));
+                uint32_t k = 0;
+                while (k < n && (pm[k] != m || pb[k] != b)) ++k;
+                if (k == n) {
+                    if (n == kSlotPairs) {
+                        fits = false;
+                        break;
+                    }
+                    pm[n] = m;
+                    pb[n] = b;
+                    ++n;
+                }
+                word_pair[w] = (uint8_t)k;
+            }
+            uint8_t *idx = slot + 8ull * kSlotPairs;
+            if (!fits) {
+                all_fit.store(false, std::memory_order_relaxed);
+                continue;
+            }
+            for (uint32_t k = 0; k < n; ++k) {
+                std::memcpy(slot + 8ull * k, &pm[k], 4);
+                std::memcpy(slot + 8ull * k + 4, &pb[k], 4);
+            }
+            for (uint32_t l = 0; l < 64; ++l)
+                for (uint32_t j = 0; j < K; ++j) {
+                    const uint32_t w = l + 64 * j;
+                    const uint32_t k = w < W ? word_pair[w] : 0u;
+                    const uint64_t bit = 4ull * (K * l + j);
+                    idx[bit >> 3] |= (uint8_t)(k << (bit & 7));
+                }
+        }
+    });
+    return all_fit.load();
+}
+
+}  // namespace ibp

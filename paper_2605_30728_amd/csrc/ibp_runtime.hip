@@ -50,6 +50,12 @@ constexpr uint64_t kCountBytes = dev::kCountLines * dev::kCountStride * 8;   // 
 constexpr uint64_t kBlk = 256;                    // rows per host packing task (a chunk
                                                   // holds tens of them, for 16 threads)
 
+// the host builds the compact metadata slots that the kernels read: one layout
+static_assert(kSlotPairs == dev::kSlotPairs, "slot layout");
+static_assert(meta_slot_bytes(1) == dev::meta_slot_bytes<1>() && meta_slot_bytes(2) == dev::meta_slot_bytes<2>() &&
+                  meta_slot_bytes(4) == dev::meta_slot_bytes<4>() && meta_slot_bytes(8) == dev::meta_slot_bytes<8>(),
+              "slot size");
+
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
 // Best-effort calls (cleanup, device restore) whose status is deliberately ignored.
@@ -77,6 +83,7 @@ struct ibp_handle {
     ibp_desc d{};
     dev::DevStream ds{};
     uint32_t *d_meta = nullptr;
+    uint8_t *d_slots = nullptr;           // compact metadata of the row gathers (clustered, W <= 512)
     uint64_t *d_index = nullptr;
     uint8_t *d_payload = nullptr;
     const uint8_t *k_payload = nullptr;   // what the kernels read: d_payload or the pinned host payload
@@ -172,6 +179,7 @@ ibp_status check_handle(ibp_handle *h, const CallScope &cs) {
 void free_handle(ibp_handle *h) {
     if (!h) return;
     ignore(hipFree(h->d_meta));
+    ignore(hipFree(h->d_slots));
     ignore(hipFree(h->d_index));
     ignore(hipFree(h->d_payload));
     ignore(hipFree(h->d_err));
@@ -461,6 +469,19 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     if (hipMemcpy(h->d_index, v.index_bytes(), 8 * n_index, hipMemcpyHostToDevice) != hipSuccess ||
         hipMemset(h->d_err, 0, 8) != hipSuccess)
         return bail(fail(IBP_EHIP, "index upload failed"));
+    const uint32_t W = d.row_bytes / 4;
+    if (d.flags == 0 && W <= 512) {
+        // the row gathers read a cluster's metadata for every row they decode: when every
+        // cluster fits one, give each a compact slot as well
+        const uint32_t K = (uint32_t)dev::words_per_lane(W);
+        std::vector<uint8_t> slots;
+        if (build_meta_slots(v.meta(), d.n_groups, W, K, *h->pool, slots)) {
+            if (hipMalloc((void **)&h->d_slots, slots.size()) != hipSuccess)
+                return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
+            if (hipMemcpy(h->d_slots, slots.data(), slots.size(), hipMemcpyHostToDevice) != hipSuccess)
+                return bail(fail(IBP_EHIP, "metadata upload failed"));
+        }
+    }
     if (flags == IBP_OPEN_PAYLOAD_DEVICE) {
         const uint64_t bytes = round_up(d.payload_bytes + kSlack, 256);
         if (hipMalloc((void **)&h->d_payload, bytes) != hipSuccess)
@@ -486,6 +507,7 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
             return bail(fail(IBP_EHIP, "event creation failed"));
     if (hipDeviceSynchronize() != hipSuccess) return bail(fail(IBP_EHIP, "upload did not complete"));
     h->ds.meta = h->d_meta;
+    h->ds.slots = h->d_slots;
     h->ds.index = h->d_index;
     h->ds.n_rows = d.n_rows;
     h->ds.n_groups = d.n_groups;
@@ -645,6 +667,8 @@ ibp_status ibp_get_stats(ibp_handle *h, ibp_stats *st) {
     clear_error();
     if (!h || !st) return fail(IBP_EINVAL, "null argument");
     *st = h->stats;
+    const uint32_t W = h->d.row_bytes / 4;
+    st->gather_meta_bytes = h->d_slots ? meta_slot_bytes((uint32_t)dev::words_per_lane(W)) : 2ull * h->d.row_bytes;
     return IBP_OK;
 }
 

@@ -6,6 +6,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include "ibp_device.hpp"
+
 namespace ibp {
 namespace dev {
 
@@ -44,22 +46,72 @@ __device__ __forceinline__ uint64_t wave_slot() {
            (uint32_t)__builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));
 }
 
-template <int K>
+// How the row gathers read a cluster's Mask/Bitval words: the raw words, or the
+// cluster's compact slot (kSlotPairs {Mask, Bitval} u32 pairs, then the 4-bit pair
+// indices, lane l's K indices in bits [4Kl, 4Kl + 4K)), used when every cluster of the
+// stream fits one.
+enum { kMetaRaw = 0, kMetaSlots = 1 };
+
+// A row's metadata as loaded: raw v[2j] = Mask, v[2j+1] = Bitval of word l + 64j; slots
+// v[0], v[1] = pair l mod kSlotPairs, v[2] = the lane's index bits.
+template <int K, int FORM>
 struct RowMeta {
-    uint32_t m[K], b[K];
+    uint32_t v[FORM == kMetaSlots ? 3 : 2 * K];
 };
 
-// Raw Mask/Bitval words of the lane's words of a row. Lanes past the row's end load a
-// valid word (clamped address) and are masked where the words are used, so the loads
-// carry no exec mask and no default value that would force earlier loads to drain.
-template <int K>
-__device__ __forceinline__ void load_row_meta(RowMeta<K> &rm, const uint32_t *__restrict__ mg, uint32_t W) {
+// Issue a row's metadata loads (every address inside the slot or clamped inside the row,
+// so none is exec-masked).
+template <int K, int FORM>
+__device__ __forceinline__ void load_row_meta(RowMeta<K, FORM> &r, const uint32_t *__restrict__ mg,
+                                              const uint8_t *__restrict__ slot, uint32_t W) {
     const uint32_t l = lane_id();
+    if constexpr (FORM == kMetaSlots) {
+        const uint2 p = reinterpret_cast<const uint2 *>(slot)[l % kSlotPairs];
+        r.v[0] = p.x;
+        r.v[1] = p.y;
+        const uint8_t *__restrict__ idx = slot + 8 * kSlotPairs;
+        if constexpr (K == 1) r.v[2] = idx[l >> 1];
+        else if constexpr (K == 2) r.v[2] = idx[l];
+        else if constexpr (K == 4) r.v[2] = reinterpret_cast<const uint16_t *>(idx)[l];
+        else r.v[2] = reinterpret_cast<const uint32_t *>(idx)[l];
+    } else {
 #pragma unroll
-    for (int j = 0; j < K; ++j) {
-        const uint32_t w = min(l + kWave * j, W - 1);
-        rm.m[j] = mg[w];
-        rm.b[j] = mg[W + w];
+        for (int j = 0; j < K; ++j) {
+            const uint32_t w = min(l + kWave * j, W - 1);
+            r.v[2 * j] = mg[w];
+            r.v[2 * j + 1] = mg[W + w];
+        }
+    }
+}
+
+// Makes the loaded words values needed at this point of the program, so the compiler
+// can neither sink the loads into the branches that use them nor interleave them with
+// the arithmetic of earlier rows: a batch's loads all leave before the first one is
+// waited for, and the batch pays one memory round trip instead of one per row.
+template <int K, int FORM>
+__device__ __forceinline__ void hold_row_meta(RowMeta<K, FORM> &r) {
+#pragma unroll
+    for (int k = 0; k < (int)(sizeof(r.v) / sizeof(r.v[0])); ++k) asm volatile("" : "+v"(r.v[k]));
+}
+
+// The lane's K Mask and Bitval words; from a slot, each word takes its pair from the
+// lane that holds it (ds_bpermute).
+template <int K, int FORM>
+__device__ __forceinline__ void expand_row_meta(const RowMeta<K, FORM> &r, uint32_t (&m)[K], uint32_t (&b)[K]) {
+    if constexpr (FORM == kMetaSlots) {
+        const uint32_t bits = K == 1 ? r.v[2] >> ((lane_id() & 1u) * 4u) : r.v[2];
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const int a = (int)(((bits >> (4 * j)) & 15u) * 4u);
+            m[j] = (uint32_t)__builtin_amdgcn_ds_bpermute(a, (int)r.v[0]);
+            b[j] = (uint32_t)__builtin_amdgcn_ds_bpermute(a, (int)r.v[1]);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            m[j] = r.v[2 * j];
+            b[j] = r.v[2 * j + 1];
+        }
     }
 }
 
