@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "libibp.so")
 ARCH = os.environ.get("IBP_OFFLOAD_ARCH", "gfx950")
 
 HIP_SOURCES = ["ibp_kernels.hip", "ibp_cache_kernels.hip", "ibp_runtime.hip"]
-CXX_SOURCES = ["ibp_host.cpp", "ibp_pool.cpp", "ibp_meta_dict.cpp"]
+CXX_SOURCES = ["ibp_host.cpp", "ibp_pool.cpp", "ibp_meta_slots.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]
 HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

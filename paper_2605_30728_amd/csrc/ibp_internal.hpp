@@ -57,7 +57,7 @@ private:
     State *st_;
 };
 
-// Compact device metadata of the clustered scheme's row gathers (ibp_meta_dict.cpp): a
+// Compact device metadata of the clustered scheme's row gathers (ibp_meta_slots.cpp): a
 // fixed-size slot per cluster (meta_slot_bytes(K) bytes, cluster g at g times that) with
 // up to kSlotPairs distinct (Mask, Bitval) pairs and a 4-bit pair index per word, laid out
 // for lanes owning K words each. Returns whether every cluster fits a slot.
