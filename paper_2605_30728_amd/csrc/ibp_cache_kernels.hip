@@ -105,10 +105,12 @@ __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView 
             nm[u][j] = in_row ? ~mw[j] : 0u;
             bv[u][j] = in_row ? bw[j] : 0u;
             cntw[j] = (uint32_t)__builtin_popcount(nm[u][j]);
-            runs = max(runs, run_count(nm[u][j]));
+            if constexpr (FORM == kMetaRaw) runs = max(runs, run_count(nm[u][j]));
         }
         const uint32_t tot = row_offsets<K>(cntw, ofs[u]);
-        const uint32_t max_runs = wave_max(runs);
+        uint32_t max_runs;
+        if constexpr (FORM == kMetaSlots) max_runs = slot_max_runs(meta[u]);
+        else max_runs = wave_max(runs);
         nh[u] = max_runs ? max_runs - 1u : 0u;
         const uint64_t rb = (tot + 7u) >> 3;
         // a select of the two buffers, not an integer address, keeps the loads global

@@ -342,15 +342,15 @@ __global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint
 }
 
 // Gather of rows that fit one tile (W <= 64*K), built for memory-level parallelism.
-// A wave owns `seg` requests (lane i loads request i's id) and decodes them RB rows at
-// a time, each row independently: its cluster's Mask/Bitval words, a wave scan of
-// popcount(~Mask) for the bit offsets, then its packed windows. The Mask/Bitval loads of
-// batch b+1 are issued before the rebuilt words of batch b are stored, so a wave keeps
-// RB rows of payload loads, RB rows of metadata loads and its stores in flight together
-// (on gfx9 the vector memory counter also counts stores and drains in order, so loads
-// issued after a batch's stores would wait for those stores as well). Rows are rebuilt
-// with the generic run walk: with a setup per row, precomputed runs would cost more than
-// they save.
+// A wave owns `seg` requests (lane i loads request i's id and cluster offset, once) and
+// decodes them RB rows at a time, each row independently: its cluster's metadata (compact
+// slot or Mask/Bitval words), a wave scan of popcount(~Mask) for the bit offsets, then its
+// packed windows. All metadata loads of a batch leave together, then all its window loads.
+// One batch per wave measured fastest at the gathers' sizes: prefetching the next batch's
+// metadata during the current batch's windows keeps its registers live through the
+// rebuild, and the lost occupancy costs more than the overlap gains. Rows are rebuilt with
+// the holes deposit: with a setup per row, precomputed runs would cost more than they
+// save.
 template <int K, int RB, bool STAGED, int FORM>
 __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint32_t *__restrict__ pay32,
                                                          const int64_t *__restrict__ ids,
@@ -441,10 +441,12 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
                     nm[u][j] = in_row ? ~mw[j] : 0u;
                     bv[u][j] = in_row ? bw[j] : 0u;
                     cntw[j] = (uint32_t)__builtin_popcount(nm[u][j]);
-                    runs = max(runs, run_count(nm[u][j]));
+                    if constexpr (FORM == kMetaRaw) runs = max(runs, run_count(nm[u][j]));
                 }
                 tot[u] = row_offsets<K>(cntw, ofs[u]);
-                const uint32_t max_runs = wave_max(runs);
+                uint32_t max_runs;
+                if constexpr (FORM == kMetaSlots) max_runs = slot_max_runs(meta[u]);
+                else max_runs = wave_max(runs);
                 nh[u] = max_runs ? max_runs - 1u : 0u;
             }
             const uint64_t rb = row_stride((tot[u] + 7u) >> 3, s.row_align);
@@ -861,6 +863,19 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
 }
 
 
+// Compute units of the current device (cached per device).
+uint32_t compute_units() {
+    static uint32_t cached[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (!cached[dev]) {
+        int cu = 0;
+        if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
+        cached[dev] = (uint32_t)cu;
+    }
+    return cached[dev];
+}
+
 }  // namespace
 
 uint64_t div_magic(uint32_t G) {
@@ -929,11 +944,17 @@ hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64
                                ids, sg, soff, n, o, seg, err);
         return hipGetLastError();
     }
-    // One batch of RB rows per wave (measured best on the 2.4M x 100 fp32 minibatch:
-    // RB = 4 at K = 2 keeps 58 VGPRs, 8 waves per SIMD; larger batches cost occupancy,
-    // smaller ones memory-level parallelism).
+    // Batches of RB rows (RB = 4 at K = 2 keeps 8 waves per SIMD; larger batches cost
+    // occupancy, smaller ones memory-level parallelism). A wave takes one batch, or two or
+    // four while that still leaves at least two waves per wave slot of the chip: measured
+    // on the gathers, 2 batches per wave gain 1% on the 164k-row GNN minibatch and 4 gain
+    // 7% on the 3.69M-row one (fewer waves to launch), while the 53k DLRM lookups, with
+    // fewer waves than slots to begin with, lose 6-60% with more than one.
     const int rb_sel = k == 1 ? 8 : (k == 2 ? 4 : (k == 4 ? 2 : 1));
-    const uint32_t seg = (uint32_t)rb_sel;
+    const uint64_t min_waves = 2ull * compute_units() * 4 * 8;
+    uint32_t nb = 1;
+    while (nb < 4 && n / ((uint64_t)rb_sel * nb * 2) >= min_waves) nb *= 2;
+    const uint32_t seg = (uint32_t)rb_sel * nb;
     const uint64_t blocks = ((n + seg - 1) / seg + kWavesPerBlock - 1) / kWavesPerBlock;
     dim3 grid((unsigned)blocks), block(kBlock);
     auto go = [&](auto kk, auto rb) {

@@ -135,6 +135,18 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
 // has r - 1 holes.
 __device__ __forceinline__ uint32_t run_count(uint32_t v) { return (uint32_t)__builtin_popcount(v & ~(v << 1)); }
 
+// Most runs of variant bits in any word of a row, from its slot: lane l holds pair
+// l mod kSlotPairs, so lanes 0-7 hold every pair of the cluster (unused entries have Mask
+// 0, one run, which never raises a row's hole count above the count of its real words).
+template <int K>
+__device__ __forceinline__ uint32_t slot_max_runs(const RowMeta<K, kMetaSlots> &r) {
+    int x = (int)run_count(~r.v[0]);
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false));  // row_shr:1
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false));  // row_shr:2
+    x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false));  // row_shr:4
+    return (uint32_t)__builtin_amdgcn_readlane(x, 7);
+}
+
 // nh is wave-uniform and at least the word's own hole count; extra iterations find no
 // hole (below = all but bit 31, width 0) and leave y as it is.
 __device__ __forceinline__ uint32_t word_deposit(uint32_t bv, uint32_t nm, uint32_t x, uint32_t nh) {
