@@ -25,6 +25,8 @@ Also reported on the same JSON line:
                 and the library's multi-threaded host compressor rate (context);
   uncompressed_device  the same steps over the rows stored uncompressed (a stream whose
                 Masks are all 0, decoded by the same kernels): the uncompressed baseline;
+  plain_gather  (gathers) the same ids through torch.index_select over the uncompressed
+                rows in HBM: the achievable line of the access pattern, for context;
   e2e           the PCIe-inclusive paths (payload in pinned host memory): host-packed
                 staging + DMA, GPU-initiated zero-copy reads, and zero-copy reads of a
                 pinned copy whose rows start on 128-byte boundaries; effective output GB/s
@@ -114,6 +116,39 @@ def measured_traffic(workload, part=False):
     if kernel_sources_sha256() != m_hash.group(1):
         return None
     return int(m_bytes.group(1))
+
+
+def plain_gather(torch, rows, steps, Wm, K, L):
+    """The achievable line of the gather's access pattern: the same steps as a plain row
+    gather of the uncompressed rows resident in HBM (torch.index_select, a library kernel,
+    not the product path): its output GB/s and its read + write GB/s."""
+    table = torch.from_numpy(rows).cuda()
+    d_units = [torch.from_numpy(u).cuda() for u in steps.units]
+    out = torch.empty((max(steps.rows), L), dtype=torch.uint8, device="cuda")
+
+    def step(k):
+        u = d_units[k % len(steps)]
+        torch.index_select(table, 0, u, out=out[:u.numel()])
+    for k in range(Wm):
+        step(k)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        step(Wm + k)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    out_bytes = sum(steps.rows[(Wm + k) % len(steps)] * L for k in range(K))
+    last = (Wm + K - 1) % len(steps)
+    ok = np.array_equal(out[:steps.rows[last]].cpu().numpy(), rows[steps.row_ids(last)])
+    del table, out, d_units
+    torch.cuda.empty_cache()
+    if not ok:
+        log("[bench] ERROR: plain gather differs from the rows")
+        sys.exit(1)
+    gbs = out_bytes / dt / 1e9
+    log(f"[bench] plain uncompressed row gather (torch.index_select, same ids): {gbs:.1f} GB/s out, "
+        f"{2 * gbs:.0f} GB/s read+write")
+    return {"GBps": round(gbs, 2), "read_write_GBps": round(2 * gbs, 1), "op": "torch.index_select"}
 
 
 def d2d_copy_gbs(torch, nbytes=1 << 30, reps=5):
@@ -694,6 +729,7 @@ def main():
     ibp.ibp_close(hu)
     log(f"[bench] same steps over uncompressed rows (device-resident): {out_bytes / wall_u / 1e9:.1f} GB/s "
         f"-> compressed is {wall_u / wall:.2f}x the uncompressed speed")
+    plain = plain_gather(torch, rows, steps, Wm, K, L) if wl in GATHERS else None
     copy_gbs = d2d_copy_gbs(torch)
     traffic = measured_traffic(wl, part)
     log(f"[bench] {K} steps in {wall * 1e3:.2f} ms: {value:.1f} GB/s decompressed; kernel {kern_ms * 1e3:.1f} us "
@@ -732,6 +768,7 @@ def main():
                      "gather_meta_bytes_per_cluster": gather_meta if wl in GATHERS else None},
         "uncompressed_device": {"GBps": round(out_bytes / wall_u / 1e9, 2),
                                 "speedup_of_compressed": round(wall_u / wall, 3)},
+        "plain_gather": plain,
         "cpu_baseline": cpu,
         "e2e": e2e,
     }
