@@ -827,6 +827,7 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         constexpr int RB = K <= 1 ? 8 : (K <= 2 ? 4 : (K <= 4 ? 2 : 1));
         const uint32_t nb = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(4, n / (16384ull * RB)));
         const uint32_t seg = RB * nb;
+        if (seg > (uint32_t)kWave) return hipErrorInvalidValue;   // lane i holds item i
         const uint64_t waves = (n + seg - 1) / seg;
         const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
         const bool pre = (s.W - 1) / s.part_m < 32u * kPreDwords;    // at most 64 chunks
@@ -955,6 +956,7 @@ hipError_t launch_gather(const DevStream &s, const uint8_t *payload, const int64
     uint32_t nb = 1;
     while (nb < 4 && n / ((uint64_t)rb_sel * nb * 2) >= min_waves) nb *= 2;
     const uint32_t seg = (uint32_t)rb_sel * nb;
+    if (seg > (uint32_t)kWave) return hipErrorInvalidValue;   // lane i holds request i
     const uint64_t blocks = ((n + seg - 1) / seg + kWavesPerBlock - 1) / kWavesPerBlock;
     dim3 grid((unsigned)blocks), block(kBlock);
     auto go = [&](auto kk, auto rb) {
