@@ -111,9 +111,9 @@ typedef struct {
     uint64_t gather_meta_bytes; /* device metadata a row gather reads per cluster it
                                 touches: a compact slot when the stream uses the clustered
                                 scheme, rows of at most 2048 bytes and every cluster
-                                repeats at most 8 distinct (Mask, Bitval) pairs over its
-                                words (128 bytes at up to 512-byte rows), else the
-                                2 * row_bytes of Mask and Bitval. A property of the
+                                repeats at most 16 distinct (Mask, Bitval) pairs over its
+                                words (128 bytes at up to 512-byte rows and 8 pairs), else
+                                the 2 * row_bytes of Mask and Bitval. A property of the
                                 handle: ibp_reset_stats leaves it */
 } ibp_stats;
 

@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView 
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
         const uint64_t g = rd64(g_l, slot_of(u));
-        load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * meta_slot_bytes<K>(), W);
+        load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * s.slot_bytes, s.slot_pairs, W);
     }
 #pragma unroll
     for (int u = 0; u < RB; ++u) hold_row_meta(meta[u]);
@@ -109,7 +109,7 @@ __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView 
         }
         const uint32_t tot = row_offsets<K>(cntw, ofs[u]);
         uint32_t max_runs;
-        if constexpr (FORM == kMetaSlots) max_runs = slot_max_runs(meta[u]);
+        if constexpr (FORM == kMetaSlots) max_runs = slot_max_runs(meta[u], s.slot_pairs);
         else max_runs = wave_max(runs);
         nh[u] = max_runs ? max_runs - 1u : 0u;
         const uint64_t rb = (tot + 7u) >> 3;

@@ -21,10 +21,13 @@ struct DevStream {
     uint32_t part_m;         // participation scheme: words per chunk; 0 = clustered scheme
     uint32_t row_align;      // clustered scheme: rows of a cluster start every
                              // roundup(rb, row_align) bytes (0: every rb bytes, no padding)
-    // clustered scheme, W <= 512, every cluster with at most kSlotPairs distinct (Mask,
-    // Bitval) pairs: the row gathers' compact metadata, one slot of meta_slot_bytes<K>()
-    // bytes per cluster (see load_row_meta); null: they read `meta`
+    // clustered scheme, W <= 512, every cluster with at most 16 distinct (Mask, Bitval)
+    // pairs: the row gathers' compact metadata, one slot of slot_bytes per cluster holding
+    // slot_pairs (8 or 16) pairs and the 4-bit word indices (see load_row_meta); slots
+    // null: they read `meta`
     const uint8_t *slots;
+    uint32_t slot_pairs;
+    uint32_t slot_bytes;
 };
 
 uint64_t div_magic(uint32_t G);
@@ -34,11 +37,9 @@ uint64_t div_magic(uint32_t G);
 // with K = 8.
 inline int words_per_lane(uint32_t W) { return W <= 64 ? 1 : W <= 128 ? 2 : W <= 256 ? 4 : 8; }
 
-// Compact metadata slot of a cluster for rows decoded with K words per lane: 8 (Mask,
-// Bitval) u32 pairs, then 32K bytes of 4-bit pair indices, padded to 128-byte lines.
-inline constexpr uint32_t kSlotPairs = 8;
-template <int K>
-inline constexpr uint32_t meta_slot_bytes() { return (8 * kSlotPairs + 32 * K + 127) / 128 * 128; }
+// Bytes of a compact metadata slot holding `pairs` (Mask, Bitval) u32 pairs and the 4-bit
+// pair indices of rows decoded with K words per lane (32K bytes), padded to 128-byte lines.
+inline constexpr uint32_t meta_slot_bytes(uint32_t pairs, uint32_t K) { return (8 * pairs + 32 * K + 127) / 128 * 128; }
 
 // Rows [first, first + n) into out (row-major). Packed row r of group g is read at byte
 // off[g] - pay_base + (r - g*G) * rb_g of `payload` (participation scheme: at byte

@@ -58,12 +58,12 @@ private:
 };
 
 // Compact device metadata of the clustered scheme's row gathers (ibp_meta_slots.cpp): a
-// fixed-size slot per cluster (meta_slot_bytes(K) bytes, cluster g at g times that) with
-// up to kSlotPairs distinct (Mask, Bitval) pairs and a 4-bit pair index per word, laid out
-// for lanes owning K words each. Returns whether every cluster fits a slot.
-constexpr uint32_t kSlotPairs = 8;
-constexpr uint64_t meta_slot_bytes(uint32_t K) { return (8ull * kSlotPairs + 32ull * K + 127) / 128 * 128; }
-bool build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32_t K, Pool &pool,
-                      std::vector<uint8_t> &slots);
+// fixed-size slot per cluster, cluster g at g * slot bytes, with its distinct (Mask, Bitval)
+// pairs (room for 8, or for 16 when some cluster has more than 8) and a 4-bit pair index per
+// word, laid out for lanes owning K words each. Returns the pairs per slot (8 or 16), or 0
+// when some cluster has more than 16 distinct pairs (no slots).
+constexpr uint64_t meta_slot_bytes(uint32_t pairs, uint32_t K) { return (8ull * pairs + 32ull * K + 127) / 128 * 128; }
+uint32_t build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32_t K, Pool &pool,
+                          std::vector<uint8_t> &slots);
 
 }  // namespace ibp

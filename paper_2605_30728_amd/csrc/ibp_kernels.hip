@@ -409,7 +409,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
             const uint64_t g = rd64(g_lo, g_hi, slot_of(base_i + u));
-            load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * meta_slot_bytes<K>(), W);
+            load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * s.slot_bytes, s.slot_pairs, W);
         }
 #pragma unroll
         for (int u = 0; u < RB; ++u) hold_row_meta(meta[u]);
@@ -445,7 +445,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
                 }
                 tot[u] = row_offsets<K>(cntw, ofs[u]);
                 uint32_t max_runs;
-                if constexpr (FORM == kMetaSlots) max_runs = slot_max_runs(meta[u]);
+                if constexpr (FORM == kMetaSlots) max_runs = slot_max_runs(meta[u], s.slot_pairs);
                 else max_runs = wave_max(runs);
                 nh[u] = max_runs ? max_runs - 1u : 0u;
             }

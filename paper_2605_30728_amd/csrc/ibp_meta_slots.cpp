@@ -1,24 +1,27 @@
 // Compact device form of the clustered scheme's Mask/Bitval words, read by the row
-// gathers (the kernel side is load_row_meta_slot / expand_row_meta in ibp_wave.hpp).
+// gathers (the kernel side is load_row_meta / expand_row_meta in ibp_wave.hpp).
 //
 // A cluster stores one (Mask_w, Bitval_w) pair per 32-bit word w (Sec. 3.2). The words of
 // a row repeat few distinct pairs (columns of one feature table share their invariant
 // exponent and mantissa bits), and a gather reads a cluster's metadata for every row it
-// decodes. So every cluster also gets a fixed-size slot, at slot_bytes(K) * g of the
-// slot area, holding
+// decodes. So every cluster also gets a fixed-size slot, at g * slot bytes of the slot
+// area, holding
 //
-//   pairs   kSlotPairs x {u32 Mask, u32 Bitval}: the cluster's distinct pairs in order of
-//           first appearance (unused entries zero)
+//   pairs   P x {u32 Mask, u32 Bitval}: the cluster's distinct pairs in order of first
+//           appearance (unused entries zero); P = 8, or 16 when some cluster of the
+//           stream has more than 8
 //   index   32*K bytes: a 4-bit pair index per word, laid out for the wave that decodes
 //           the row: lane l owns words l, l+64, ..., l+64*(K-1) and their K indices sit
 //           together in bits [4*K*l, 4*K*l + 4*K) of the area (index j in bits 4j..4j+3
 //           of that field), so a lane fetches all of its indices with one load
 //
-// Words past the row's end (lanes of the last tile) take index 0. A slot's address
-// follows from the cluster number alone, so its loads need nothing but the row id; at
-// K <= 2 a slot is one 128-byte line, against 8W bytes of raw metadata. The kernels read
-// slots only when every cluster of the stream fits one (a per-row choice of form would
-// cost every row a branch); otherwise the slots are dropped and the raw words are read.
+// padded to whole 128-byte lines. Words past the row's end (lanes of the last tile) take
+// index 0. A slot's address follows from the cluster number alone, so its loads need
+// nothing but the row id; at K <= 2 and P = 8 a slot is one 128-byte line, against 8W
+// bytes of raw metadata. The kernels read slots only when every cluster of the stream
+// fits one (a per-row choice of form would cost every row a branch); a stream with a
+// cluster of more than 16 pairs gets no slots and the raw words are read.
+#include <algorithm>
 #include <atomic>
 #include <cstring>
 
@@ -28,50 +31,68 @@ namespace ibp {
 
 namespace {
 
+constexpr uint32_t kMaxPairs = 16;   // 4-bit indices
+
 inline uint32_t rd32(const uint8_t *p) {
     uint32_t v;
     std::memcpy(&v, p, 4);
     return v;
 }
 
+// Distinct (Mask, Bitval) pairs of the cluster at mg, in order of first appearance, and
+// each word's pair index; stops (returning kMaxPairs + 1) at the first pair beyond
+// kMaxPairs.
+uint32_t cluster_pairs(const uint8_t *mg, uint32_t W, uint32_t *pm, uint32_t *pb, uint8_t *word_pair) {
+    uint32_t n = 0;
+    for (uint32_t w = 0; w < W; ++w) {
+        const uint32_t m = rd32(mg + 4ull * w), b = rd32(mg + 4ull * (W + w));
+        uint32_t k = 0;
+        while (k < n && (pm[k] != m || pb[k] != b)) ++k;
+        if (k == n) {
+            if (n == kMaxPairs) return kMaxPairs + 1;
+            pm[n] = m;
+            pb[n] = b;
+            ++n;
+        }
+        if (word_pair) word_pair[w] = (uint8_t)k;
+    }
+    return n;
+}
+
 }  // namespace
 
-bool build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32_t K, Pool &pool,
-                      std::vector<uint8_t> &slots) {
-    std::atomic<bool> all_fit{true};
-    const uint64_t S = meta_slot_bytes(K), raw = 8ull * W;
+uint32_t build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32_t K, Pool &pool,
+                          std::vector<uint8_t> &slots) {
+    const uint64_t raw = 8ull * W;
+    // pass 1: the most distinct pairs of any cluster
+    std::atomic<uint32_t> most{0};
+    pool.run(n_groups, 1024, [&](uint64_t lo, uint64_t hi) {
+        uint32_t pm[kMaxPairs], pb[kMaxPairs], m = 0;
+        for (uint64_t g = lo; g < hi && m <= kMaxPairs; ++g)
+            m = std::max(m, cluster_pairs(meta + g * raw, W, pm, pb, nullptr));
+        uint32_t cur = most.load(std::memory_order_relaxed);
+        while (m > cur && !most.compare_exchange_weak(cur, m, std::memory_order_relaxed)) {
+        }
+    });
+    const uint32_t P = most.load() <= 8 ? 8u : most.load() <= kMaxPairs ? kMaxPairs : 0u;
+    if (!P) {
+        slots.clear();
+        return 0;
+    }
+    const uint64_t S = meta_slot_bytes(P, K);
     slots.assign(std::max<uint64_t>(n_groups * S, 8), 0);
+    // pass 2: the slots
     pool.run(n_groups, 1024, [&](uint64_t lo, uint64_t hi) {
         std::vector<uint8_t> word_pair(W);
+        uint32_t pm[kMaxPairs], pb[kMaxPairs];
         for (uint64_t g = lo; g < hi; ++g) {
-            const uint8_t *mg = meta + g * raw;
             uint8_t *slot = slots.data() + g * S;
-            uint32_t pm[kSlotPairs], pb[kSlotPairs], n = 0;
-            bool fits = true;
-            for (uint32_t w = 0; w < W && fits; ++w) {
-                const uint32_t m = rd32(mg + 4ull * w), b = rd32(mg + 4ull * (W + w));
-                uint32_t k = 0;
-                while (k < n && (pm[k] != m || pb[k] != b)) ++k;
-                if (k == n) {
-                    if (n == kSlotPairs) {
-                        fits = false;
-                        break;
-                    }
-                    pm[n] = m;
-                    pb[n] = b;
-                    ++n;
-                }
-                word_pair[w] = (uint8_t)k;
-            }
-            uint8_t *idx = slot + 8ull * kSlotPairs;
-            if (!fits) {
-                all_fit.store(false, std::memory_order_relaxed);
-                continue;
-            }
+            const uint32_t n = cluster_pairs(meta + g * raw, W, pm, pb, word_pair.data());
             for (uint32_t k = 0; k < n; ++k) {
                 std::memcpy(slot + 8ull * k, &pm[k], 4);
                 std::memcpy(slot + 8ull * k + 4, &pb[k], 4);
             }
+            uint8_t *idx = slot + 8ull * P;
             for (uint32_t l = 0; l < 64; ++l)
                 for (uint32_t j = 0; j < K; ++j) {
                     const uint32_t w = l + 64 * j;
@@ -81,7 +102,7 @@ bool build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32
                 }
         }
     });
-    return all_fit.load();
+    return P;
 }
 
 }  // namespace ibp

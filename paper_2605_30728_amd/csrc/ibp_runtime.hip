@@ -51,9 +51,9 @@ constexpr uint64_t kBlk = 256;                    // rows per host packing task 
                                                   // holds tens of them, for 16 threads)
 
 // the host builds the compact metadata slots that the kernels read: one layout
-static_assert(kSlotPairs == dev::kSlotPairs, "slot layout");
-static_assert(meta_slot_bytes(1) == dev::meta_slot_bytes<1>() && meta_slot_bytes(2) == dev::meta_slot_bytes<2>() &&
-                  meta_slot_bytes(4) == dev::meta_slot_bytes<4>() && meta_slot_bytes(8) == dev::meta_slot_bytes<8>(),
+static_assert(meta_slot_bytes(8, 1) == dev::meta_slot_bytes(8, 1) && meta_slot_bytes(8, 2) == dev::meta_slot_bytes(8, 2) &&
+                  meta_slot_bytes(16, 4) == dev::meta_slot_bytes(16, 4) &&
+                  meta_slot_bytes(16, 8) == dev::meta_slot_bytes(16, 8),
               "slot size");
 
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
@@ -475,11 +475,14 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
         // cluster fits one, give each a compact slot as well
         const uint32_t K = (uint32_t)dev::words_per_lane(W);
         std::vector<uint8_t> slots;
-        if (build_meta_slots(v.meta(), d.n_groups, W, K, *h->pool, slots)) {
+        const uint32_t P = build_meta_slots(v.meta(), d.n_groups, W, K, *h->pool, slots);
+        if (P) {
             if (hipMalloc((void **)&h->d_slots, slots.size()) != hipSuccess)
                 return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
             if (hipMemcpy(h->d_slots, slots.data(), slots.size(), hipMemcpyHostToDevice) != hipSuccess)
                 return bail(fail(IBP_EHIP, "metadata upload failed"));
+            h->ds.slot_pairs = P;
+            h->ds.slot_bytes = (uint32_t)meta_slot_bytes(P, K);
         }
     }
     if (flags == IBP_OPEN_PAYLOAD_DEVICE) {
@@ -667,8 +670,7 @@ ibp_status ibp_get_stats(ibp_handle *h, ibp_stats *st) {
     clear_error();
     if (!h || !st) return fail(IBP_EINVAL, "null argument");
     *st = h->stats;
-    const uint32_t W = h->d.row_bytes / 4;
-    st->gather_meta_bytes = h->d_slots ? meta_slot_bytes((uint32_t)dev::words_per_lane(W)) : 2ull * h->d.row_bytes;
+    st->gather_meta_bytes = h->d_slots ? h->ds.slot_bytes : 2ull * h->d.row_bytes;
     return IBP_OK;
 }
 

@@ -47,13 +47,13 @@ __device__ __forceinline__ uint64_t wave_slot() {
 }
 
 // How the row gathers read a cluster's Mask/Bitval words: the raw words, or the
-// cluster's compact slot (kSlotPairs {Mask, Bitval} u32 pairs, then the 4-bit pair
+// cluster's compact slot (P = 8 or 16 {Mask, Bitval} u32 pairs, then the 4-bit pair
 // indices, lane l's K indices in bits [4Kl, 4Kl + 4K)), used when every cluster of the
 // stream fits one.
 enum { kMetaRaw = 0, kMetaSlots = 1 };
 
 // A row's metadata as loaded: raw v[2j] = Mask, v[2j+1] = Bitval of word l + 64j; slots
-// v[0], v[1] = pair l mod kSlotPairs, v[2] = the lane's index bits.
+// v[0], v[1] = pair l mod P, v[2] = the lane's index bits.
 template <int K, int FORM>
 struct RowMeta {
     uint32_t v[FORM == kMetaSlots ? 3 : 2 * K];
@@ -63,13 +63,13 @@ struct RowMeta {
 // so none is exec-masked).
 template <int K, int FORM>
 __device__ __forceinline__ void load_row_meta(RowMeta<K, FORM> &r, const uint32_t *__restrict__ mg,
-                                              const uint8_t *__restrict__ slot, uint32_t W) {
+                                              const uint8_t *__restrict__ slot, uint32_t P, uint32_t W) {
     const uint32_t l = lane_id();
     if constexpr (FORM == kMetaSlots) {
-        const uint2 p = reinterpret_cast<const uint2 *>(slot)[l % kSlotPairs];
+        const uint2 p = reinterpret_cast<const uint2 *>(slot)[l & (P - 1)];
         r.v[0] = p.x;
         r.v[1] = p.y;
-        const uint8_t *__restrict__ idx = slot + 8 * kSlotPairs;
+        const uint8_t *__restrict__ idx = slot + 8 * P;
         if constexpr (K == 1) r.v[2] = idx[l >> 1];
         else if constexpr (K == 2) r.v[2] = idx[l];
         else if constexpr (K == 4) r.v[2] = reinterpret_cast<const uint16_t *>(idx)[l];
@@ -135,16 +135,17 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
 // has r - 1 holes.
 __device__ __forceinline__ uint32_t run_count(uint32_t v) { return (uint32_t)__builtin_popcount(v & ~(v << 1)); }
 
-// Most runs of variant bits in any word of a row, from its slot: lane l holds pair
-// l mod kSlotPairs, so lanes 0-7 hold every pair of the cluster (unused entries have Mask
-// 0, one run, which never raises a row's hole count above the count of its real words).
+// Most runs of variant bits in any word of a row, from its slot of P (8 or 16) pairs: lane
+// l holds pair l mod P, so lanes 0 .. P-1 hold every pair of the cluster (unused entries
+// have Mask 0, one run, which never raises a row's hole count above that of its words).
 template <int K>
-__device__ __forceinline__ uint32_t slot_max_runs(const RowMeta<K, kMetaSlots> &r) {
+__device__ __forceinline__ uint32_t slot_max_runs(const RowMeta<K, kMetaSlots> &r, uint32_t P) {
     int x = (int)run_count(~r.v[0]);
     x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false));  // row_shr:1
     x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false));  // row_shr:2
     x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false));  // row_shr:4
-    return (uint32_t)__builtin_amdgcn_readlane(x, 7);
+    if (P > 8) x = max(x, __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false));  // row_shr:8
+    return (uint32_t)__builtin_amdgcn_readlane(x, (int)P - 1);
 }
 
 // nh is wave-uniform and at least the word's own hole count; extra iterations find no

@@ -1,9 +1,9 @@
-"""GPU parity of the row gathers across the two forms of cluster metadata they read: the
-compact slots (every cluster's words repeat at most 8 distinct (Mask, Bitval) pairs) and
-the raw Mask/Bitval words (some cluster has more). Clusters are drawn with a chosen
-number of distinct pairs, up to the boundary (slots) or across it (raw), for every tile
-width (1, 2, 4 and 8 words per lane) and a ragged last cluster; expected rows come from
-the CPU oracle."""
+"""GPU parity of the row gathers across the forms of cluster metadata they read: compact
+slots with room for 8 pairs (every cluster's words repeat at most 8 distinct (Mask,
+Bitval) pairs), for 16 (some cluster has 9-16), and the raw Mask/Bitval words (some
+cluster has more). Clusters are drawn with a chosen number of distinct pairs, up to each
+boundary and across it, for every tile width (1, 2, 4 and 8 words per lane) and a ragged
+last cluster; expected rows come from the CPU oracle."""
 import sys
 
 import numpy as np
@@ -14,7 +14,7 @@ import paper_2605_30728_amd as ibp
 
 pytestmark = pytest.mark.gpu
 
-SETS = {"fit": [1, 2, 7, 8, 3], "mixed": [1, 2, 7, 8, 9, 16, 40]}
+SETS = {"fit": [1, 2, 7, 8, 3], "fit16": [1, 9, 16, 12, 3], "mixed": [1, 2, 7, 8, 9, 16, 40]}
 
 
 def say(*a):
@@ -66,7 +66,7 @@ def distinct_pairs(rows, G, W):
 
 @pytest.mark.parametrize("W", [16, 64, 100, 128, 200, 256, 500, 512])
 @pytest.mark.parametrize("mode", ["device_ids", "host_ids", "host_payload", "zero_copy", "cache"])
-@pytest.mark.parametrize("pairs", ["fit", "mixed"])
+@pytest.mark.parametrize("pairs", ["fit", "fit16", "mixed"])
 def test_gather_both_metadata_forms(torch, W, mode, pairs):
     G = 32
     n = G * len(SETS[pairs]) * 2 + 5
@@ -75,8 +75,11 @@ def test_gather_both_metadata_forms(torch, W, mode, pairs):
     counts = distinct_pairs(rows, G, W)
     if pairs == "fit":
         assert max(counts) <= 8 and 8 in counts, counts
+    elif pairs == "fit16":
+        assert max(counts) == 16 and 9 in counts, counts
     else:
-        assert 8 in counts and 9 in counts, counts
+        assert 8 in counts and 9 in counts and (W <= 16 or max(counts) > 16), counts
+    room = 8 if max(counts) <= 8 else 16 if max(counts) <= 16 else None
     stream = oracle.compress(rows, G)
     rng = np.random.default_rng(W + 1)
     ids = np.concatenate([np.sort(rng.integers(0, n, size=3 * n)), rng.integers(0, n, size=n),
@@ -90,11 +93,11 @@ def test_gather_both_metadata_forms(torch, W, mode, pairs):
     out = torch.full((ids.size * L + 256,), 0xA5, dtype=torch.uint8, device="cuda")
     d_ids = torch.from_numpy(ids).cuda()
     with ibp.ibp_open(stream, 0, flags) as h:
-        # slots (8 pairs of 8 bytes and 32K bytes of indices, in 128-byte lines) only
-        # when every cluster fits one
+        # slots (8 or 16 pairs of 8 bytes and 32K bytes of indices, in 128-byte lines)
+        # only when every cluster fits one
         k = 1 if W <= 64 else 2 if W <= 128 else 4 if W <= 256 else 8
-        slot = (64 + 32 * k + 127) // 128 * 128
-        assert ibp.ibp_get_stats(h)["gather_meta_bytes"] == (slot if pairs == "fit" else 2 * L)
+        want_meta = 2 * L if room is None else (8 * room + 32 * k + 127) // 128 * 128
+        assert ibp.ibp_get_stats(h)["gather_meta_bytes"] == want_meta
         if mode == "cache":
             with ibp.ibp_cache_create(h, np.arange(0, n, 3)) as c:
                 ibp.ibp_cache_gather(c, d_ids, out, out_cap=ids.size * L)
