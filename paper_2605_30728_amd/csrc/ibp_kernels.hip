@@ -23,6 +23,7 @@
 //     two dwords at its bit offset and funnel-shifted (v_alignbit_b32), never with
 //     sub-dword loads. No MFMA anywhere: nothing here is a contraction.
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "ibp_device.hpp"
@@ -864,17 +865,20 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
 }
 
 
-// Compute units of the current device (cached per device).
+// Compute units of the current device (cached per device; concurrent first calls store
+// the same value).
 uint32_t compute_units() {
-    static uint32_t cached[64] = {};
+    static std::atomic<uint32_t> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (!cached[dev]) {
-        int cu = 0;
-        if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0) cu = 256;
-        cached[dev] = (uint32_t)cu;
+    uint32_t cu = cached[dev].load(std::memory_order_relaxed);
+    if (!cu) {
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+        cu = (uint32_t)v;
+        cached[dev].store(cu, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return cu;
 }
 
 }  // namespace
