@@ -637,16 +637,23 @@ __global__ __launch_bounds__(kBlock) void k_part_rows(DevStream s, const uint32_
     }
 }
 
-// RB participation-scheme rows of one cluster (tile t), one tile each (W <= 64K): the
-// participation dwords of all RB rows are loaded together, then every row's widths, scan
-// and two-dword windows, then the rebuilt words are stored. Loads are unconditional with
-// clamped addresses (inside the row or the readable slack), so no exec-masked load makes
-// earlier loads drain.
-template <int NR, int RB, bool PRE, int K, int MAXR>
-__device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
-                                           const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
-                                           const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
-                                           uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords]) {
+// RB participation-scheme rows of one cluster (tile t), one tile each (W <= 64K), in two
+// stages. part_batch_load: the participation dwords of all RB rows are loaded together (or
+// were prefetched with the lookup), then every row's widths, scan and two-dword windows.
+// part_batch_rebuild: the rebuilt words. Between the two the caller stores the previous
+// batch, so those stores leave after this batch's window loads and the compiler never
+// waits for them before reusing registers. Loads are unconditional with clamped addresses
+// (inside the row or the readable slack), so no exec-masked load makes earlier loads drain.
+template <int RB, int K>
+struct PartLoads {
+    uint32_t d0[RB][K], d1[RB][K], b[RB][K], pb[RB][K];
+};
+
+template <int RB, bool PRE, int K, int MAXR>
+__device__ __forceinline__ void part_batch_load(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                                const uint64_t (&rbyte)[RB], const bool (&raw)[RB], uint32_t m,
+                                                uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords],
+                                                PartLoads<RB, K> &ld) {
     const uint32_t l = lane_id();
     uint32_t pd[RB];
     if constexpr (!PRE) {
@@ -658,7 +665,6 @@ __device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_
             pd[u] = __builtin_amdgcn_alignbit(p[ql + 1], p[ql], ((uint32_t)rbyte[u] & 3u) * 8u);
         }
     }
-    uint32_t d0[RB][K], d1[RB][K], b[RB][K], pb[RB][K];
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
         uint32_t width[K];
@@ -669,8 +675,8 @@ __device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_
             uint32_t dw;
             if constexpr (PRE) dw = (c >> 5) ? pds[u][1] : pds[u][0];
             else dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((c >> 5) & 63u) * 4u), (int)pd[u]);
-            pb[u][j] = raw[u] ? 0u : (dw >> (c & 31u)) & 1u;
-            width[j] = w < W ? (pb[u][j] ? (uint32_t)__builtin_popcount(t.nm[j]) : 32u) : 0u;
+            ld.pb[u][j] = raw[u] ? 0u : (dw >> (c & 31u)) & 1u;
+            width[j] = w < W ? (ld.pb[u][j] ? (uint32_t)__builtin_popcount(t.nm[j]) : 32u) : 0u;
         }
         const uint32_t *__restrict__ p = pay32 + (rbyte[u] >> 2);
         const uint32_t start = ((uint32_t)rbyte[u] & 3u) * 8u + (raw[u] ? 0u : C);
@@ -678,48 +684,99 @@ __device__ __forceinline__ void part_batch(const Tile<K, MAXR> &t, const uint32_
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const uint32_t inc = wave_incl_scan(width[j]);
-            b[u][j] = start + c + inc - width[j];
+            ld.b[u][j] = start + c + inc - width[j];
             c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
-            d0[u][j] = p[b[u][j] >> 5];
-            d1[u][j] = p[(b[u][j] >> 5) + 1];
+            ld.d0[u][j] = p[ld.b[u][j] >> 5];
+            ld.d1[u][j] = p[(ld.b[u][j] >> 5) + 1];
         }
     }
+}
+
+template <int NR, int RB, int K, int MAXR>
+__device__ __forceinline__ void part_batch_rebuild(const Tile<K, MAXR> &t, const PartLoads<RB, K> &ld,
+                                                   uint32_t (&v)[RB][K]) {
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-            const uint32_t x = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], b[u][j]);
-            uint32_t v;
-            if constexpr (NR >= 0) v = word_fast<NR>(t, j, x);
-            else v = word_generic(t.bv[j], t.nm[j], x);
-            v = pb[u][j] ? v : x;
-            const uint32_t w = l + kWave * j;
-            if (ok[u] && w < W) orow[u][w] = v;
+            const uint32_t x = __builtin_amdgcn_alignbit(ld.d1[u][j], ld.d0[u][j], ld.b[u][j]);
+            uint32_t y;
+            if constexpr (NR >= 0) y = word_fast<NR>(t, j, x);
+            else y = word_generic(t.bv[j], t.nm[j], x);
+            v[u][j] = ld.pb[u][j] ? y : x;
         }
     }
 }
 
-template <int RB, bool PRE, int K, int MAXR>
-__device__ __forceinline__ void part_batch_any(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
-                                               const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
-                                               const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
-                                               uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords]) {
-    switch (t.nr) {   // wave-uniform
-    case 0: part_batch<0, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return;
-    case 1: part_batch<1, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return;
-    case 2: if constexpr (MAXR >= 2) { part_batch<2, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return; } break;
-    case 3: if constexpr (MAXR >= 3) { part_batch<3, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return; } break;
-    case 4: if constexpr (MAXR >= 4) { part_batch<4, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds); return; } break;
-    default: break;
-    }
-    part_batch<-1, RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds);
+// Rebuilt words of RB rows waiting to be stored.
+template <int RB, int K>
+struct PartPending {
+    uint32_t v[RB][K];
+    uint32_t *orow[RB];
+    bool ok[RB];
+    bool any = false;
+};
+
+template <int RB, int K>
+__device__ __forceinline__ void part_store(PartPending<RB, K> &pp, uint32_t W) {
+    if (!pp.any) return;
+    const uint32_t l = lane_id();
+#pragma unroll
+    for (int u = 0; u < RB; ++u)
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t w = l + kWave * j;
+            if (pp.ok[u] && w < W) pp.orow[u][w] = pp.v[u][j];
+        }
+    pp.any = false;
 }
 
-// Participation-scheme rows that fit one tile (W <= 64K), in batches of RB rows. A wave
+// One batch: its loads, then (DEFER) the previous batch's stores, its rebuild, and
+// (otherwise) its own stores. The run count is a template parameter of the whole step, so
+// each variant keeps only its own registers live.
+template <int NR, int RB, bool PRE, bool DEFER, int K, int MAXR>
+__device__ __forceinline__ void part_batch_step(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                                const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
+                                                const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
+                                                uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords],
+                                                PartPending<RB, K> &pend) {
+    PartLoads<RB, K> ld;
+    part_batch_load<RB, PRE>(t, pay32, rbyte, raw, m, C, W, pds, ld);
+    if constexpr (DEFER) part_store(pend, W);
+    part_batch_rebuild<NR>(t, ld, pend.v);
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+        pend.orow[u] = orow[u];
+        pend.ok[u] = ok[u];
+    }
+    pend.any = true;
+    if constexpr (!DEFER) part_store(pend, W);
+}
+
+template <int RB, bool PRE, bool DEFER, int K, int MAXR>
+__device__ __forceinline__ void part_batch_step_any(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
+                                                    const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
+                                                    const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
+                                                    uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords],
+                                                    PartPending<RB, K> &pend) {
+    switch (t.nr) {   // wave-uniform
+    case 0: part_batch_step<0, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return;
+    case 1: part_batch_step<1, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return;
+    case 2: if constexpr (MAXR >= 2) { part_batch_step<2, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return; } break;
+    case 3: if constexpr (MAXR >= 3) { part_batch_step<3, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return; } break;
+    case 4: if constexpr (MAXR >= 4) { part_batch_step<4, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return; } break;
+    default: break;
+    }
+    part_batch_step<-1, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend);
+}
+
+// Participation-scheme rows that fit one tile (W <= 64K), in batches of RB rows. With
+// DEFER (a wave of several batches) each batch's stores wait until the next batch's
+// window loads have left; one batch per wave stores at once and keeps fewer registers. A wave
 // owns `seg` (<= 64) work items; lane i < seg first locates item i (its cluster, the
 // byte of its row and its size), then batches of RB rows are decoded with part_batch
 // while they share a cluster (always, under one global Mask), else row by row.
-template <int K, int MAXR, int RB, int SRC, bool PRE>
+template <int K, int MAXR, int RB, int SRC, bool PRE, bool DEFER>
 __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint32_t *__restrict__ pay32,
                                                           uint64_t pay_base, const int64_t *__restrict__ ids,
                                                           const uint32_t *__restrict__ sg,
@@ -776,6 +833,7 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
     };
     Tile<K, MAXR> t;
     uint64_t cached_g = ~0ull;
+    PartPending<RB, K> pend;
     for (uint32_t i = 0; i < cnt; i += RB) {
         uint64_t rbyte[RB];
         bool raw[RB], ok[RB];
@@ -799,11 +857,13 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
         }
         if (same) {
             if (g0 != cached_g) {
+                part_store(pend, W);
                 tile_setup(t, s.meta + g0 * 2ull * W, W, 0, 0);
                 cached_g = g0;
             }
-            part_batch_any<RB, PRE>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds);
+            part_batch_step_any<RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend);
         } else {
+            part_store(pend, W);
 #pragma unroll
             for (int u = 0; u < RB; ++u) {
                 if (!ok[u]) continue;
@@ -816,6 +876,7 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
             }
         }
     }
+    part_store(pend, W);
 }
 
 template <int K, int MAXR>
@@ -832,20 +893,24 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         const uint64_t waves = (n + seg - 1) / seg;
         const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
         const bool pre = (s.W - 1) / s.part_m < 32u * kPreDwords;    // at most 64 chunks
-        auto go = [&](auto pre_tag) {
-            constexpr bool P = decltype(pre_tag)::value;
+        auto go = [&](auto pre_tag, auto defer_tag) {
+            constexpr bool P = decltype(pre_tag)::value, D = decltype(defer_tag)::value;
             if (ids)
-                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds, P>), grid, block, 0, stream, s, p, pay_base,
-                                   ids, sg, soff, first, n, o, seg, err);
+                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds, P, D>), grid, block, 0, stream, s, p,
+                                   pay_base, ids, sg, soff, first, n, o, seg, err);
             else if (sg)
-                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcStaged, P>), grid, block, 0, stream, s, p,
+                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcStaged, P, D>), grid, block, 0, stream, s, p,
                                    pay_base, ids, sg, soff, first, n, o, seg, err);
             else
-                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcRange, P>), grid, block, 0, stream, s, p,
+                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcRange, P, D>), grid, block, 0, stream, s, p,
                                    pay_base, ids, sg, soff, first, n, o, seg, err);
         };
-        if (pre) go(std::true_type{});
-        else go(std::false_type{});
+        auto go_pre = [&](auto defer_tag) {
+            if (pre) go(std::true_type{}, defer_tag);
+            else go(std::false_type{}, defer_tag);
+        };
+        if (nb > 1) go_pre(std::true_type{});
+        else go_pre(std::false_type{});
         return hipGetLastError();
     }
     // rows of several tiles: one row at a time per wave
