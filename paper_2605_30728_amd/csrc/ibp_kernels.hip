@@ -404,6 +404,26 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
     // loads stay in bounds and their stores are skipped)
     auto slot_of = [&](uint32_t i) { return i < cnt ? i : cnt - 1; };
     const uint32_t nb = (cnt + RB - 1) / RB;
+    // rebuilt words of the previous batch: stored once the next batch's metadata loads have
+    // left, so waiting for that metadata never waits for those stores
+    uint32_t pv[RB][K];
+    uint32_t pbase = 0;
+    bool pending = false;
+    auto store_pending = [&]() {
+        if (!pending) return;
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
+            const uint32_t i = pbase + u;
+            const bool row_ok = i < cnt && !((bad >> (i & 63)) & 1ull);
+            uint32_t *__restrict__ orow = out_seg + (uint64_t)slot_of(i) * W;
+#pragma unroll
+            for (int j = 0; j < K; ++j) {
+                const uint32_t w = l + kWave * j;
+                if (row_ok && w < W) orow[w] = pv[u][j];
+            }
+        }
+        pending = false;
+    };
     for (uint32_t bb = 0; bb < nb; ++bb) {
         const uint32_t base_i = bb * RB;
         RowMeta<K, FORM> meta[RB];
@@ -412,6 +432,7 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
             const uint64_t g = rd64(g_lo, g_hi, slot_of(base_i + u));
             load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * s.slot_bytes, s.slot_pairs, W);
         }
+        store_pending();
 #pragma unroll
         for (int u = 0; u < RB; ++u) hold_row_meta(meta[u]);
         // per row: variant positions, Bitval, bit offsets of the words inside the packed
@@ -474,18 +495,13 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
             for (int j = 0; j < K; ++j)
                 x[u][j] = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], ofs[u][j] + bit0[u]);
 #pragma unroll
-        for (int u = 0; u < RB; ++u) {
-            const uint32_t i = base_i + u;
-            const bool row_ok = i < cnt && !((bad >> (i & 63)) & 1ull);
-            uint32_t *__restrict__ orow = out_seg + (uint64_t)slot_of(i) * W;
+        for (int u = 0; u < RB; ++u)
 #pragma unroll
-            for (int j = 0; j < K; ++j) {
-                const uint32_t v = word_deposit(bv[u][j], nm[u][j], x[u][j], nh[u]);
-                const uint32_t w = l + kWave * j;
-                if (row_ok && w < W) orow[w] = v;
-            }
-        }
+            for (int j = 0; j < K; ++j) pv[u][j] = word_deposit(bv[u][j], nm[u][j], x[u][j], nh[u]);
+        pbase = base_i;
+        pending = true;
     }
+    store_pending();
 }
 
 // ---- the thresholded scheme with participation bits (stream flags = 1) ----------
