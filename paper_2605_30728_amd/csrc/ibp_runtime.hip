@@ -336,11 +336,24 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
     const uint32_t *grb = h->h_rb.data();
     const uint64_t *hoff = h->h_off.data();
     const bool part = h->d.flags & IBP_STREAM_PARTICIPATION;
+    // the range check of every id rides on this pass (no extra serial pass over the ids);
+    // the first bad position is reported before anything is enqueued
+    const uint64_t n_rows = h->d.n_rows;
+    std::atomic<uint64_t> first_bad{n};
     h->pool->run(nblk_all, 1, [&](uint64_t lo, uint64_t hi) {
         for (uint64_t k = lo; k < hi; ++k) {
             uint64_t sum = 0;
             for (uint64_t i = k * blk, e = std::min(n, i + blk); i < e; ++i) {
                 const uint64_t id = (uint64_t)ids[i];
+                if (id >= n_rows) {   // negative ids wrap to large values
+                    uint64_t cur = first_bad.load(std::memory_order_relaxed);
+                    while (i < cur && !first_bad.compare_exchange_weak(cur, i, std::memory_order_relaxed)) {
+                    }
+                    rg[i] = 0;
+                    rsrc[i] = 0;
+                    rrb[i] = 0;
+                    continue;
+                }
                 const uint64_t g = G == 1 ? id : (uint64_t)(((unsigned __int128)id * magic) >> 64);
                 rg[i] = (uint32_t)g;
                 if (part) {
@@ -355,6 +368,9 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
             bs[k + 1] = sum;
         }
     });
+    if (const uint64_t i = first_bad.load(); i < n)
+        return fail(IBP_ERANGE, "row id " + std::to_string(ids[i]) + " at position " + std::to_string(i) +
+                                    " is outside [0, " + std::to_string(n_rows) + ")");
     for (uint64_t i0 = 0; i0 < n; i0 += per_chunk) {
         const uint64_t nc = std::min(per_chunk, n - i0);
         const int b = h->next_stage;
@@ -597,13 +613,13 @@ ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t
     if (n_ids == 0) return IBP_OK;
     if (!row_ids || !d_out) return fail(IBP_EINVAL, "row ids or output is null");
     if (out_cap / d.row_bytes < n_ids) return fail(IBP_ENOMEM, "output capacity too small");
-    for (uint64_t i = 0; i < n_ids; ++i)
-        if (row_ids[i] < 0 || (uint64_t)row_ids[i] >= d.n_rows)
-            return fail(IBP_ERANGE, "row id " + std::to_string(row_ids[i]) + " at position " + std::to_string(i) +
-                                        " is outside [0, " + std::to_string(d.n_rows) + ")");
     hipStream_t s = static_cast<hipStream_t>(stream);
     const uint64_t L = d.row_bytes;
     if (h->flags != IBP_OPEN_PAYLOAD_HOST) {
+        for (uint64_t i = 0; i < n_ids; ++i)
+            if (row_ids[i] < 0 || (uint64_t)row_ids[i] >= d.n_rows)
+                return fail(IBP_ERANGE, "row id " + std::to_string(row_ids[i]) + " at position " + std::to_string(i) +
+                                            " is outside [0, " + std::to_string(d.n_rows) + ")");
         const int j = h->next_ids;
         st = claim_ids(h, j, n_ids);
         if (st != IBP_OK) return st;
