@@ -71,7 +71,8 @@ SMALL = [("floats", 300, 400, 32), ("random", 97, 12, 5), ("specials", 70, 16, 7
          ("sparse", 129, 256, 32), ("alternating", 80, 24, 8), ("identical", 66, 20, 16),
          ("smallint", 33, 4, 32), ("onebit", 50, 36, 1), ("floats", 200, 516, 100),
          ("sparse", 90, 1024, 32), ("floats", 70, 2400, 16), ("floats", 61, 260, 64),
-         ("alternating", 45, 520, 9), ("floats", 40, 4096, 32), ("random", 19, 4096, 8)]
+         ("alternating", 45, 520, 9), ("floats", 40, 4096, 32), ("random", 19, 4096, 8),
+         ("floats", 300, 400, 300), ("sparse", 90, 256, 1000)]
 
 
 @pytest.mark.parametrize("flags", ["device", "host", "zero_copy", "zero_copy_aligned"])
