@@ -136,7 +136,7 @@ __global__ __launch_bounds__(kBlock) void k_cache_gather(DevStream s, CacheView 
             const uint32_t x = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], ofs[u][j] + bit0[u]);
             const uint32_t v = word_deposit(bv[u][j], nm[u][j], x, nh[u]);
             const uint32_t w = l + kWave * j;
-            if (row_ok && w < W) orow[w] = v;
+            if (row_ok && w < W) store_out(&orow[w], v);
         }
     }
 }

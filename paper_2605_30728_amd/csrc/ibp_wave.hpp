@@ -115,6 +115,13 @@ __device__ __forceinline__ void expand_row_meta(const RowMeta<K, FORM> &r, uint3
     }
 }
 
+// Store of a gathered output word that no later step of the kernel reads: marked
+// non-temporal, so a gather's output stream does not evict the metadata slots and packed
+// rows that neighbouring requests are about to read from L2 (measured: 7% on 53k Zipf
+// lookups, whose hot rows repeat across waves; the contiguous decompress keeps plain
+// stores, which measured 7% faster there).
+__device__ __forceinline__ void store_out(uint32_t *p, uint32_t v) { __builtin_nontemporal_store(v, p); }
+
 // Maximum over the 64 lanes of a wave (DPP, as the scan), result in every lane's SGPR.
 __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
     int x = (int)v;
