@@ -1,8 +1,9 @@
 """GPU parity over a seeded random sweep of shapes: row widths from 1 to 700 words, cluster
 sizes from 1 to past the row count, every value structure of the test generators, both
 schemes, every payload placement, ranges and gathers with duplicates, unsorted ids and
-ragged tails. Each case decodes the oracle's stream on the GPU and compares every row, bit
-for bit, with the oracle's bit-serial decode (and the original rows)."""
+ragged tails, and the compressed cache on zero-copy handles. Each case decodes the oracle's
+stream on the GPU and compares every row, bit for bit, with the oracle's bit-serial decode
+(and the original rows)."""
 import sys
 
 import numpy as np
@@ -87,4 +88,16 @@ def test_random_case(torch, k):
         got = out[:ids.size * L].cpu().numpy().reshape(ids.size, L)
         assert (out[ids.size * L:].cpu().numpy() == 0xA5).all(), "gather wrote past its rows"
         assert np.array_equal(got, want_ids)
+        if flags == ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY and not part and W <= 512:
+            # the compressed cache over the same handle: a random third of the rows cached
+            cached = np.flatnonzero(rng.random(n) < 1 / 3)
+            out.fill_(0xA5)
+            with ibp.ibp_cache_create(h, cached) as c:
+                ibp.ibp_cache_gather(c, torch.from_numpy(ids).cuda(), out, out_cap=ids.size * L)
+                torch.cuda.synchronize()
+                st = ibp.ibp_cache_get_stats(c)
+            got = out[:ids.size * L].cpu().numpy().reshape(ids.size, L)
+            assert np.array_equal(got, want_ids)
+            hits = int(np.isin(ids, cached).sum())
+            assert st["hits"] == hits and st["misses"] == ids.size - hits
         assert ibp.ibp_device_errors(h) == 0
