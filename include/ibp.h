@@ -122,9 +122,9 @@ enum {
     IBP_OPEN_PAYLOAD_DEVICE = 0, /* copied to device memory (HBM) once, at open */
     IBP_OPEN_PAYLOAD_HOST = 1,   /* kept in library-owned pinned host memory; every call
                                     moves the needed packed bytes over PCIe through
-                                    rotating 64 MiB staging buffers on a side stream (the
+                                    rotating 128 MiB staging buffers on a side stream (the
                                     host packs the rows of a gather); rows of at most
-                                    64 MiB - 72 bytes */
+                                    128 MiB - 72 bytes */
     IBP_OPEN_PAYLOAD_HOST_ZERO_COPY = 2, /* kept in library-owned pinned host memory and read
                                     by the decode kernels themselves over PCIe
                                     (GPU-initiated transfers, Sec. 4.4): no host packing,

@@ -42,7 +42,9 @@ namespace ibp {
 namespace {
 
 constexpr uint64_t kSlack = 256;                 // readable bytes past any payload end
-constexpr uint64_t kStageBytes = 64ull << 20;    // one staging buffer
+constexpr uint64_t kStageBytes = 128ull << 20;   // one staging buffer (a whole compressed 128 MiB
+                                                  // KV layer in one copy: 0.98 of CR x raw H2D,
+                                                  // against 0.85 in two 64 MiB copies)
 constexpr int kStages = 3;                        // staging buffers in rotation
 constexpr int kIdSlots = 2;                       // host-id buffers in rotation
 constexpr uint64_t kRowAlign = 128;               // PCIe line: row start of aligned zero-copy

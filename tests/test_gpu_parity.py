@@ -211,8 +211,9 @@ def _sampled_groups_match_oracle(stream, rows, G, L, n_groups, n_sample, seed):
         assert np.array_equal(pay, o[od:]), g
 
 
-@pytest.mark.parametrize("kind,n,L,G", [("random", 40000, 4096, 32), ("floats", 600000, 400, 32),
-                                         ("sparse", 300000, 512, 64)])
+# packed bytes of 2.5-3 staging buffers of 128 MiB: ~4,096, ~199 and ~464 B per packed row
+@pytest.mark.parametrize("kind,n,L,G", [("random", 84000, 4096, 32), ("floats", 1700000, 400, 32),
+                                         ("sparse", 730000, 512, 64)])
 def test_staged_multi_chunk(torch, kind, n, L, G):
     """Ranges whose packed bytes span several staging buffers on the pinned-host path, cut
     at arbitrary rows (chunk ends fall inside clusters), starting and ending mid-cluster."""
@@ -418,13 +419,13 @@ def test_aligned_zero_copy_rejects_participation_streams(torch):
 
 
 def test_host_placement_rejects_rows_larger_than_a_stage(torch):
-    """A row that cannot fit one 64 MiB staging buffer is refused at open for the staged
+    """A row that cannot fit one 128 MiB staging buffer is refused at open for the staged
     placement (and accepted by the others)."""
-    L = 64 << 20
+    L = 128 << 20
     rows = np.zeros((1, L), np.uint8)
     rows[0, ::4097] = 7
     stream = ibp.ibp_compress(rows, 1)
-    say("[edge] 64 MiB row on the staged placement")
+    say("[edge] 128 MiB row on the staged placement")
     with pytest.raises(ibp.IbpError) as e:
         ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_HOST)
     assert e.value.status == ibp.IBP_EINVAL
