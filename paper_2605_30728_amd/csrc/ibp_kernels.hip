@@ -41,6 +41,7 @@ struct Tile {
     uint32_t bv[K];          // Bitval of the lane's words
     uint32_t nm[K];          // ~Mask: the variant positions
     uint32_t s[K];           // bit offset of the word inside the packed row
+    uint32_t pk[K];          // packed width popcount(~Mask) (0 past the row's end)
     uint32_t rot[K][MAXR];   // rotate-right amount that lands run k at its position
     uint32_t rm[K][MAXR];    // run k's bits in place
     uint32_t bits;           // packed bits of this tile (wave-uniform)
@@ -63,6 +64,7 @@ __device__ __forceinline__ void tile_setup(Tile<K, MAXR> &t, const uint32_t *__r
         t.nm[j] = ~m;
         t.bv[j] = b;
         const uint32_t n = (uint32_t)__builtin_popcount(~m);
+        t.pk[j] = n;
         const uint32_t inc = wave_incl_scan(n);
         t.s[j] = c + inc - n;
         c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
@@ -515,10 +517,6 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
 
 enum { kSrcRange = 0, kSrcIds = 1, kSrcStaged = 2 };
 
-// Rows of at most 32 * kPreDwords chunks take their participation dwords together with
-// their lookup (one round trip per wave instead of one per batch).
-constexpr int kPreDwords = 2;
-
 // Decode one tile (words [w0, w0 + 64K)) of one participation-scheme row whose bytes
 // start at byte `rbyte` of pay32; `start` is the bit of the row where this tile's first
 // word begins. Returns the tile's bits.
@@ -654,56 +652,88 @@ __global__ __launch_bounds__(kBlock) void k_part_rows(DevStream s, const uint32_
 }
 
 // RB participation-scheme rows of one cluster (tile t), one tile each (W <= 64K), in two
-// stages. part_batch_load: the participation dwords of all RB rows are loaded together (or
-// were prefetched with the lookup), then every row's widths, scan and two-dword windows.
+// stages. part_batch_load: the participation bits of all RB rows (loaded together, or
+// prefetched with the lookup), then every row's widths, scan and two-dword windows.
 // part_batch_rebuild: the rebuilt words. Between the two the caller stores the previous
 // batch, so those stores leave after this batch's window loads and the compiler never
 // waits for them before reusing registers. Loads are unconditional with clamped addresses
 // (inside the row or the readable slack), so no exec-masked load makes earlier loads drain.
+//
+// Everything a batch knows about its rows is wave-uniform and read on demand from the
+// lanes of the lookup (lane i holds item i): a row's byte offset and prefetched
+// participation dwords by readlane, whether it is raw or to be stored from bit masks. A
+// row's chunk bit becomes an all-ones or all-zeros lane mask (a sign-extended bit-field
+// extract), which then selects the word's width and its rebuilt or raw value by bitfield
+// insert, with no compare and no branch per row. PRE: 0 = the participation dwords are
+// loaded per batch, 1 or 2 = that many dwords were prefetched (at most 32 or 64 chunks).
 template <int RB, int K>
 struct PartLoads {
-    uint32_t d0[RB][K], d1[RB][K], b[RB][K], pb[RB][K];
+    uint32_t d0[RB][K], d1[RB][K];
+    uint32_t bs[RB][K];   // bits 0-4: the window's shift; bits 5-31: all ones when the chunk is compressed
 };
 
-template <int RB, bool PRE, int K, int MAXR>
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, uint32_t i) {
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), (int)i) << 32) |
+           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, (int)i);
+}
+
+// m ? a : b, bit by bit, in one instruction (written out, the compiler splits it into a
+// not, an and and an and-or, and keeps every row's inverted mask live)
+__device__ __forceinline__ uint32_t bit_select(uint32_t m, uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(m), "v"(a), "v"(b));
+    return r;
+}
+
+template <int RB, int PRE, int K, int MAXR>
 __device__ __forceinline__ void part_batch_load(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
-                                                const uint64_t (&rbyte)[RB], const bool (&raw)[RB], uint32_t m,
-                                                uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords],
-                                                PartLoads<RB, K> &ld) {
+                                                uint64_t bit_l, const uint32_t (&pdw)[2], uint32_t i,
+                                                uint32_t last, uint64_t rawm, uint32_t m, uint32_t C, uint32_t W,
+                                                const uint32_t (&full)[K], PartLoads<RB, K> &ld) {
     const uint32_t l = lane_id();
     uint32_t pd[RB];
-    if constexpr (!PRE) {
+    if constexpr (PRE == 0) {
         const uint32_t nd = (((W - 1) / m) >> 5) + 1;
         const uint32_t ql = min(l, nd - 1);
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
-            const uint32_t *__restrict__ p = pay32 + (rbyte[u] >> 2);
-            pd[u] = __builtin_amdgcn_alignbit(p[ql + 1], p[ql], ((uint32_t)rbyte[u] & 3u) * 8u);
+            const uint32_t iu = min(i + u, last);
+            const uint32_t raw = (uint32_t)(rawm >> iu) & 1u;
+            const uint64_t pbit = lane_u64(bit_l, iu) - (raw ? 0u : C);   // the row's first bit
+            const uint32_t *__restrict__ p = pay32 + (pbit >> 5);
+            const uint32_t d = __builtin_amdgcn_alignbit(p[ql + 1], p[ql], (uint32_t)pbit & 31u);
+            pd[u] = d & (raw - 1u);   // raw rows: no chunk is compressed
         }
     }
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
-        uint32_t width[K];
+        const uint32_t iu = min(i + u, last);
+        const uint64_t rbit = lane_u64(bit_l, iu);
+        uint32_t d_lo = 0, d_hi = 0;
+        if constexpr (PRE >= 1) d_lo = (uint32_t)__builtin_amdgcn_readlane((int)pdw[0], (int)iu);
+        if constexpr (PRE >= 2) d_hi = (uint32_t)__builtin_amdgcn_readlane((int)pdw[1], (int)iu);
+        uint32_t width[K], sel[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const uint32_t w = l + kWave * j;
             const uint32_t c = (w < W ? w : 0u) / m;
             uint32_t dw;
-            if constexpr (PRE) dw = (c >> 5) ? pds[u][1] : pds[u][0];
-            else dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((c >> 5) & 63u) * 4u), (int)pd[u]);
-            ld.pb[u][j] = raw[u] ? 0u : (dw >> (c & 31u)) & 1u;
-            width[j] = w < W ? (ld.pb[u][j] ? (uint32_t)__builtin_popcount(t.nm[j]) : 32u) : 0u;
+            if constexpr (PRE == 0) dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((c >> 5) & 63u) * 4u), (int)pd[u]);
+            else if constexpr (PRE == 1) dw = d_lo;
+            else dw = (c >> 5) ? d_hi : d_lo;
+            sel[j] = (uint32_t)__builtin_amdgcn_sbfe((int)dw, c & 31u, 1u);   // 0 or ~0
+            width[j] = bit_select(sel[j], t.pk[j], full[j]);
         }
-        const uint32_t *__restrict__ p = pay32 + (rbyte[u] >> 2);
-        const uint32_t start = ((uint32_t)rbyte[u] & 3u) * 8u + (raw[u] ? 0u : C);
-        uint32_t c = 0;
+        const uint32_t *__restrict__ p = pay32 + (rbit >> 5);
+        uint32_t c = (uint32_t)rbit & 31u;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const uint32_t inc = wave_incl_scan(width[j]);
-            ld.b[u][j] = start + c + inc - width[j];
-            c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
-            ld.d0[u][j] = p[ld.b[u][j] >> 5];
-            ld.d1[u][j] = p[(ld.b[u][j] >> 5) + 1];
+            const uint32_t b = c + inc - width[j];
+            if (j + 1 < K) c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+            ld.d0[u][j] = p[b >> 5];
+            ld.d1[u][j] = p[(b >> 5) + 1];
+            ld.bs[u][j] = bit_select(31u, b, sel[j]);
         }
     }
 }
@@ -715,75 +745,88 @@ __device__ __forceinline__ void part_batch_rebuild(const Tile<K, MAXR> &t, const
     for (int u = 0; u < RB; ++u) {
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-            const uint32_t x = __builtin_amdgcn_alignbit(ld.d1[u][j], ld.d0[u][j], ld.b[u][j]);
+            const uint32_t x = __builtin_amdgcn_alignbit(ld.d1[u][j], ld.d0[u][j], ld.bs[u][j]);
             uint32_t y;
             if constexpr (NR >= 0) y = word_fast<NR>(t, j, x);
             else y = word_generic(t.bv[j], t.nm[j], x);
-            v[u][j] = ld.pb[u][j] ? y : x;
+            v[u][j] = bit_select((uint32_t)((int32_t)ld.bs[u][j] >> 31), y, x);
         }
     }
 }
 
-// Rebuilt words of RB rows waiting to be stored.
+// Rebuilt words of RB rows waiting to be stored: rows row0 .. row0 + RB - 1 of the wave's
+// output, row row0 + u stored when bit u of `ok` is set (both wave-uniform).
 template <int RB, int K>
 struct PartPending {
     uint32_t v[RB][K];
-    uint32_t *orow[RB];
-    bool ok[RB];
-    bool any = false;
+    uint32_t row0 = 0;
+    uint32_t ok = 0;
 };
 
 template <int RB, int K>
-__device__ __forceinline__ void part_store(PartPending<RB, K> &pp, uint32_t W) {
-    if (!pp.any) return;
+__device__ __forceinline__ void part_store(PartPending<RB, K> &pp, uint32_t *__restrict__ out_seg, uint32_t W) {
+    if (!pp.ok) return;
     const uint32_t l = lane_id();
 #pragma unroll
-    for (int u = 0; u < RB; ++u)
+    for (int u = 0; u < RB; ++u) {
+        if (!((pp.ok >> u) & 1u)) continue;
+        uint32_t *__restrict__ orow = out_seg + (uint64_t)(pp.row0 + u) * W;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             const uint32_t w = l + kWave * j;
-            if (pp.ok[u] && w < W) store_out(&pp.orow[u][w], pp.v[u][j]);
+            if (w < W) store_out(&orow[w], pp.v[u][j]);
         }
-    pp.any = false;
+    }
+    pp.ok = 0;
+}
+
+// Store what is pending and drop the words: on paths that set up a tile or decode row by
+// row, the words are then not kept live (the compiler cannot tell that `ok` is zero).
+template <int RB, int K>
+__device__ __forceinline__ void part_flush(PartPending<RB, K> &pp, uint32_t *__restrict__ out_seg, uint32_t W) {
+    part_store(pp, out_seg, W);
+#pragma unroll
+    for (int u = 0; u < RB; ++u)
+#pragma unroll
+        for (int j = 0; j < K; ++j) pp.v[u][j] = 0u;
 }
 
 // One batch: its loads, then (DEFER) the previous batch's stores, its rebuild, and
 // (otherwise) its own stores. The run count is a template parameter of the whole step, so
 // each variant keeps only its own registers live.
-template <int NR, int RB, bool PRE, bool DEFER, int K, int MAXR>
+template <int NR, int RB, int PRE, bool DEFER, int K, int MAXR>
 __device__ __forceinline__ void part_batch_step(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
-                                                const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
-                                                const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
-                                                uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords],
+                                                uint64_t bit_l, const uint32_t (&pdw)[2], uint32_t i,
+                                                uint32_t last, uint64_t rawm, uint32_t ok, uint32_t m, uint32_t C,
+                                                uint32_t W, const uint32_t (&full)[K], uint32_t *__restrict__ out_seg,
                                                 PartPending<RB, K> &pend) {
     PartLoads<RB, K> ld;
-    part_batch_load<RB, PRE>(t, pay32, rbyte, raw, m, C, W, pds, ld);
-    if constexpr (DEFER) part_store(pend, W);
+    part_batch_load<RB, PRE>(t, pay32, bit_l, pdw, i, last, rawm, m, C, W, full, ld);
+    if constexpr (DEFER) part_store(pend, out_seg, W);
     part_batch_rebuild<NR>(t, ld, pend.v);
-#pragma unroll
-    for (int u = 0; u < RB; ++u) {
-        pend.orow[u] = orow[u];
-        pend.ok[u] = ok[u];
-    }
-    pend.any = true;
-    if constexpr (!DEFER) part_store(pend, W);
+    pend.row0 = i;
+    pend.ok = ok;
+    if constexpr (!DEFER) part_store(pend, out_seg, W);
 }
 
-template <int RB, bool PRE, bool DEFER, int K, int MAXR>
+template <int RB, int PRE, bool DEFER, int K, int MAXR>
 __device__ __forceinline__ void part_batch_step_any(const Tile<K, MAXR> &t, const uint32_t *__restrict__ pay32,
-                                                    const uint64_t (&rbyte)[RB], const bool (&raw)[RB],
-                                                    const bool (&ok)[RB], uint32_t *const (&orow)[RB], uint32_t m,
-                                                    uint32_t C, uint32_t W, const uint32_t (&pds)[RB][kPreDwords],
-                                                    PartPending<RB, K> &pend) {
+                                                    uint64_t bit_l, const uint32_t (&pdw)[2], uint32_t i,
+                                                    uint32_t last, uint64_t rawm, uint32_t ok, uint32_t m,
+                                                    uint32_t C, uint32_t W, const uint32_t (&full)[K],
+                                                    uint32_t *__restrict__ out_seg, PartPending<RB, K> &pend) {
+#define IBP_PART_STEP(NR) \
+    part_batch_step<NR, RB, PRE, DEFER>(t, pay32, bit_l, pdw, i, last, rawm, ok, m, C, W, full, out_seg, pend)
     switch (t.nr) {   // wave-uniform
-    case 0: part_batch_step<0, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return;
-    case 1: part_batch_step<1, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return;
-    case 2: if constexpr (MAXR >= 2) { part_batch_step<2, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return; } break;
-    case 3: if constexpr (MAXR >= 3) { part_batch_step<3, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return; } break;
-    case 4: if constexpr (MAXR >= 4) { part_batch_step<4, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend); return; } break;
+    case 0: IBP_PART_STEP(0); return;
+    case 1: IBP_PART_STEP(1); return;
+    case 2: if constexpr (MAXR >= 2) { IBP_PART_STEP(2); return; } break;
+    case 3: if constexpr (MAXR >= 3) { IBP_PART_STEP(3); return; } break;
+    case 4: if constexpr (MAXR >= 4) { IBP_PART_STEP(4); return; } break;
     default: break;
     }
-    part_batch_step<-1, RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend);
+    IBP_PART_STEP(-1);
+#undef IBP_PART_STEP
 }
 
 // Participation-scheme rows that fit one tile (W <= 64K), in batches of RB rows. With
@@ -792,7 +835,7 @@ __device__ __forceinline__ void part_batch_step_any(const Tile<K, MAXR> &t, cons
 // owns `seg` (<= 64) work items; lane i < seg first locates item i (its cluster, the
 // byte of its row and its size), then batches of RB rows are decoded with part_batch
 // while they share a cluster (always, under one global Mask), else row by row.
-template <int K, int MAXR, int RB, int SRC, bool PRE, bool DEFER>
+template <int K, int MAXR, int RB, int SRC, int PRE, bool DEFER>
 __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint32_t *__restrict__ pay32,
                                                           uint64_t pay_base, const int64_t *__restrict__ ids,
                                                           const uint32_t *__restrict__ sg,
@@ -827,15 +870,28 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
     }
     // few chunks: each lane fetches its own row's participation dwords now, in one round
     // trip for the whole segment
-    uint32_t pdw[kPreDwords] = {};
-    if constexpr (PRE) {
+    uint32_t pdw[2] = {0u, 0u};
+    if constexpr (PRE >= 1) {
         const uint32_t *__restrict__ p = pay32 + (byte_l >> 2);
         const uint32_t b0 = ((uint32_t)byte_l & 3u) * 8u;
-        const uint32_t q0 = p[0], q1 = p[1], q2 = p[2];
+        const uint32_t q0 = p[0], q1 = p[1];
         pdw[0] = __builtin_amdgcn_alignbit(q1, q0, b0);
-        pdw[1] = __builtin_amdgcn_alignbit(q2, q1, b0);
+        if constexpr (PRE >= 2) pdw[1] = __builtin_amdgcn_alignbit(p[2], q1, b0);
     }
+    // the wave's items as bit masks: bad ids, raw rows, rows to store, and rows that share
+    // the previous item's cluster (lanes past the end repeat the last item, so they do)
+    const bool raw_l = size_l == 4ull * W;
     const uint64_t bad = __ballot(l < cnt && !valid);
+    const uint64_t rawm = __ballot(raw_l);
+    // each item's first data bit in the payload, past its participation bits; a raw row
+    // has no compressed chunk
+    const uint64_t bit_l = byte_l * 8u + (raw_l ? 0u : C);
+    if (raw_l) pdw[0] = pdw[1] = 0u;
+    const uint64_t okm = __ballot(l < cnt && valid);
+    const uint32_t src = (l ? l - 1u : 0u) * 4u;
+    const uint32_t gp_lo = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)(uint32_t)g_l);
+    const uint32_t gp_hi = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)(uint32_t)(g_l >> 32));
+    const uint64_t samep = __ballot((((uint64_t)gp_hi << 32) | gp_lo) == g_l);
     uint32_t *__restrict__ out_seg = out + i0 * W;
     if (bad) {
         for (uint32_t i = 0; i < cnt; ++i)
@@ -843,56 +899,42 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
                 for (uint32_t w = l; w < W; w += kWave) out_seg[(uint64_t)i * W + w] = 0u;
         if (l == 0) atomicAdd(err, (unsigned long long)__popcll(bad));
     }
-    auto rd64 = [](uint64_t v, uint32_t i) -> uint64_t {
-        return ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), (int)i) << 32) |
-               (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, (int)i);
-    };
+    uint32_t full[K];   // a word's width when its chunk is stored raw (0 past the row's end)
+#pragma unroll
+    for (int j = 0; j < K; ++j) full[j] = l + kWave * j < W ? 32u : 0u;
+    constexpr uint64_t kTail = (1ull << (RB - 1)) - 1ull;   // rows 1 .. RB-1 of a batch
     Tile<K, MAXR> t;
     uint64_t cached_g = ~0ull;
     PartPending<RB, K> pend;
     for (uint32_t i = 0; i < cnt; i += RB) {
-        uint64_t rbyte[RB];
-        bool raw[RB], ok[RB];
-        uint32_t *orow[RB];
-        uint32_t pds[RB][kPreDwords];
-        const uint64_t g0 = rd64(g_l, i);
-        bool same = true;
-#pragma unroll
-        for (int u = 0; u < RB; ++u) {
-            const uint32_t iu = min(i + u, cnt - 1);
-            if constexpr (PRE) {
-#pragma unroll
-                for (int k = 0; k < kPreDwords; ++k)
-                    pds[u][k] = (uint32_t)__builtin_amdgcn_readlane((int)pdw[k], (int)iu);
-            }
-            rbyte[u] = rd64(byte_l, iu);
-            raw[u] = rd64(size_l, iu) == 4ull * W;
-            ok[u] = i + u < cnt && !((bad >> iu) & 1ull);
-            orow[u] = out_seg + (uint64_t)iu * W;
-            same = same && rd64(g_l, iu) == g0;
-        }
-        if (same) {
+        const uint64_t g0 = lane_u64(g_l, i);
+        const uint32_t ok = (uint32_t)(okm >> i) & ((1u << RB) - 1u);
+        const uint64_t tail = RB > 1 ? kTail << (i + 1) : 0ull;   // i + RB <= seg <= 64
+        if ((samep & tail) == tail) {
             if (g0 != cached_g) {
-                part_store(pend, W);
+                part_flush(pend, out_seg, W);
                 tile_setup(t, s.meta + g0 * 2ull * W, W, 0, 0);
                 cached_g = g0;
             }
-            part_batch_step_any<RB, PRE, DEFER>(t, pay32, rbyte, raw, ok, orow, m, C, W, pds, pend);
+            part_batch_step_any<RB, PRE, DEFER>(t, pay32, bit_l, pdw, i, cnt - 1, rawm, ok, m, C, W, full,
+                                                out_seg, pend);
         } else {
-            part_store(pend, W);
+            part_flush(pend, out_seg, W);
 #pragma unroll
             for (int u = 0; u < RB; ++u) {
-                if (!ok[u]) continue;
-                const uint64_t gu = rd64(g_l, i + u);
+                if (!((ok >> u) & 1u)) continue;
+                const uint64_t gu = lane_u64(g_l, i + u);
                 if (gu != cached_g) {
                     tile_setup(t, s.meta + gu * 2ull * W, W, 0, 0);
                     cached_g = gu;
                 }
-                part_tile_any(t, pay32, rbyte[u], raw[u], m, raw[u] ? 0u : C, W, 0, orow[u]);
+                const bool raw = (rawm >> (i + u)) & 1ull;
+                const uint64_t rbyte = (lane_u64(bit_l, i + u) - (raw ? 0u : C)) >> 3;
+                part_tile_any(t, pay32, rbyte, raw, m, raw ? 0u : C, W, 0, out_seg + (uint64_t)(i + u) * W);
             }
         }
     }
-    part_store(pend, W);
+    part_store(pend, out_seg, W);
 }
 
 template <int K, int MAXR>
@@ -908,9 +950,13 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         if (seg > (uint32_t)kWave) return hipErrorInvalidValue;   // lane i holds item i
         const uint64_t waves = (n + seg - 1) / seg;
         const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
-        const bool pre = (s.W - 1) / s.part_m < 32u * kPreDwords;    // at most 64 chunks
+        // participation dwords prefetched with the lookup: 1 for at most 32 chunks, 2 for
+        // at most 64, else loaded per batch
+        const uint32_t chunks = s.W / s.part_m;
+        const int pre = chunks <= 32u ? 1 : (chunks <= 64u ? 2 : 0);
         auto go = [&](auto pre_tag, auto defer_tag) {
-            constexpr bool P = decltype(pre_tag)::value, D = decltype(defer_tag)::value;
+            constexpr int P = decltype(pre_tag)::value;
+            constexpr bool D = decltype(defer_tag)::value;
             if (ids)
                 hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds, P, D>), grid, block, 0, stream, s, p,
                                    pay_base, ids, sg, soff, first, n, o, seg, err);
@@ -922,11 +968,18 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
                                    pay_base, ids, sg, soff, first, n, o, seg, err);
         };
         auto go_pre = [&](auto defer_tag) {
-            if (pre) go(std::true_type{}, defer_tag);
-            else go(std::false_type{}, defer_tag);
+            if (pre == 1) go(std::integral_constant<int, 1>{}, defer_tag);
+            else if (pre == 2) go(std::integral_constant<int, 2>{}, defer_tag);
+            else go(std::integral_constant<int, 0>{}, defer_tag);
         };
-        if (nb > 1) go_pre(std::true_type{});
-        else go_pre(std::false_type{});
+        // deferred stores pay at one word per lane; wider rows need the registers more
+        // (measured: 4% faster at K = 1, 15% slower at K = 2)
+        if constexpr (K == 1) {
+            if (nb > 1) go_pre(std::true_type{});
+            else go_pre(std::false_type{});
+        } else {
+            go_pre(std::false_type{});
+        }
         return hipGetLastError();
     }
     // rows of several tiles: one row at a time per wave
