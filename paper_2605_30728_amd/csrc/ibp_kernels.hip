@@ -835,8 +835,8 @@ __device__ __forceinline__ void part_batch_step_any(const Tile<K, MAXR> &t, cons
 // owns `seg` (<= 64) work items; lane i < seg first locates item i (its cluster, the
 // byte of its row and its size), then batches of RB rows are decoded with part_batch
 // while they share a cluster (always, under one global Mask), else row by row.
-template <int K, int MAXR, int RB, int SRC, int PRE, bool DEFER>
-__global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint32_t *__restrict__ pay32,
+template <int K, int MAXR, int RB, int SRC, int PRE, bool DEFER, bool ONE>
+__global__ __launch_bounds__(kBlock, (ONE && (K == 1 || (K == 2 && PRE != 0))) ? 8 : 1) void k_part_batched(DevStream s, const uint32_t *__restrict__ pay32,
                                                           uint64_t pay_base, const int64_t *__restrict__ ids,
                                                           const uint32_t *__restrict__ sg,
                                                           const uint32_t *__restrict__ soff, uint64_t first,
@@ -888,10 +888,13 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
     const uint64_t bit_l = byte_l * 8u + (raw_l ? 0u : C);
     if (raw_l) pdw[0] = pdw[1] = 0u;
     const uint64_t okm = __ballot(l < cnt && valid);
-    const uint32_t src = (l ? l - 1u : 0u) * 4u;
-    const uint32_t gp_lo = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)(uint32_t)g_l);
-    const uint32_t gp_hi = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)(uint32_t)(g_l >> 32));
-    const uint64_t samep = __ballot((((uint64_t)gp_hi << 32) | gp_lo) == g_l);
+    uint64_t samep = ~0ull;
+    if constexpr (!ONE) {
+        const uint32_t src = (l ? l - 1u : 0u) * 4u;
+        const uint32_t gp_lo = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)(uint32_t)g_l);
+        const uint32_t gp_hi = (uint32_t)__builtin_amdgcn_ds_bpermute((int)src, (int)(uint32_t)(g_l >> 32));
+        samep = __ballot((((uint64_t)gp_hi << 32) | gp_lo) == g_l);
+    }
     uint32_t *__restrict__ out_seg = out + i0 * W;
     if (bad) {
         for (uint32_t i = 0; i < cnt; ++i)
@@ -902,10 +905,21 @@ __global__ __launch_bounds__(kBlock) void k_part_batched(DevStream s, const uint
     uint32_t full[K];   // a word's width when its chunk is stored raw (0 past the row's end)
 #pragma unroll
     for (int j = 0; j < K; ++j) full[j] = l + kWave * j < W ? 32u : 0u;
-    constexpr uint64_t kTail = (1ull << (RB - 1)) - 1ull;   // rows 1 .. RB-1 of a batch
     Tile<K, MAXR> t;
-    uint64_t cached_g = ~0ull;
     PartPending<RB, K> pend;
+    if constexpr (ONE) {
+        // one cluster for the whole stream (the scheme's single global Mask)
+        tile_setup(t, s.meta, W, 0, 0);
+        for (uint32_t i = 0; i < cnt; i += RB) {
+            const uint32_t ok = (uint32_t)(okm >> i) & ((1u << RB) - 1u);
+            part_batch_step_any<RB, PRE, DEFER>(t, pay32, bit_l, pdw, i, cnt - 1, rawm, ok, m, C, W, full,
+                                                out_seg, pend);
+        }
+        part_store(pend, out_seg, W);
+        return;
+    }
+    constexpr uint64_t kTail = (1ull << (RB - 1)) - 1ull;   // rows 1 .. RB-1 of a batch
+    uint64_t cached_g = ~0ull;
     for (uint32_t i = 0; i < cnt; i += RB) {
         const uint64_t g0 = lane_u64(g_l, i);
         const uint32_t ok = (uint32_t)(okm >> i) & ((1u << RB) - 1u);
@@ -954,18 +968,24 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         // at most 64, else loaded per batch
         const uint32_t chunks = s.W / s.part_m;
         const int pre = chunks <= 32u ? 1 : (chunks <= 64u ? 2 : 0);
+        const bool one = (uint64_t)s.G >= s.n_rows;   // a single cluster
         auto go = [&](auto pre_tag, auto defer_tag) {
             constexpr int P = decltype(pre_tag)::value;
             constexpr bool D = decltype(defer_tag)::value;
-            if (ids)
-                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds, P, D>), grid, block, 0, stream, s, p,
-                                   pay_base, ids, sg, soff, first, n, o, seg, err);
-            else if (sg)
-                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcStaged, P, D>), grid, block, 0, stream, s, p,
-                                   pay_base, ids, sg, soff, first, n, o, seg, err);
-            else
-                hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcRange, P, D>), grid, block, 0, stream, s, p,
-                                   pay_base, ids, sg, soff, first, n, o, seg, err);
+            auto go_one = [&](auto one_tag) {
+                constexpr bool O = decltype(one_tag)::value;
+                if (ids)
+                    hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcIds, P, D, O>), grid, block, 0, stream, s,
+                                       p, pay_base, ids, sg, soff, first, n, o, seg, err);
+                else if (sg)
+                    hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcStaged, P, D, O>), grid, block, 0, stream,
+                                       s, p, pay_base, ids, sg, soff, first, n, o, seg, err);
+                else
+                    hipLaunchKernelGGL((k_part_batched<K, MAXR, RB, kSrcRange, P, D, O>), grid, block, 0, stream,
+                                       s, p, pay_base, ids, sg, soff, first, n, o, seg, err);
+            };
+            if (one) go_one(std::true_type{});
+            else go_one(std::false_type{});
         };
         auto go_pre = [&](auto defer_tag) {
             if (pre == 1) go(std::integral_constant<int, 1>{}, defer_tag);
