@@ -968,6 +968,7 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         // at most 64, else loaded per batch
         const uint32_t chunks = s.W / s.part_m;
         const int pre = chunks <= 32u ? 1 : (chunks <= 64u ? 2 : 0);
+        if (K == 1 && pre == 0) return hipErrorInvalidValue;   // W <= 64 words: at most 64 chunks
         const bool one = (uint64_t)s.G >= s.n_rows;   // a single cluster
         auto go = [&](auto pre_tag, auto defer_tag) {
             constexpr int P = decltype(pre_tag)::value;
@@ -990,7 +991,7 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         auto go_pre = [&](auto defer_tag) {
             if (pre == 1) go(std::integral_constant<int, 1>{}, defer_tag);
             else if (pre == 2) go(std::integral_constant<int, 2>{}, defer_tag);
-            else go(std::integral_constant<int, 0>{}, defer_tag);
+            else if constexpr (K > 1) go(std::integral_constant<int, 0>{}, defer_tag);   // K = 1: at most 64 chunks
         };
         // deferred stores pay at one word per lane; wider rows need the registers more
         // (measured: 4% faster at K = 1, 15% slower at K = 2)

@@ -120,6 +120,39 @@ def test_participation_library_stream(torch):
         assert np.array_equal(_rows(out, 5000, 400), rows)
 
 
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("G,cs", [(32, 4), (32, 8), (0, 8)], ids=["G32-C4", "G32-C8", "global-C8"])
+def test_participation_deferred_batches(torch, G, cs):
+    """Rows of one word per lane (256 B) in launches large enough for several batches per
+    wave (deferred stores): per-cluster Masks, where batches straddle clusters and decode
+    row by row, and one global Mask; 64 and 32 chunks per row (two and one participation
+    dwords fetched with the lookup). Range decode from an unaligned first row with a ragged
+    count, gathers of random and of sorted ids; every row checked against the original rows,
+    a sample of the stream against the oracle."""
+    n, L = 270_000, 256
+    rows = structured_rows("floats", n, L, seed=77)
+    s = ibp.ibp_compress_ex(rows, G or n, cs, (4, 5), 1)
+    sample = np.random.default_rng(5).choice(n, 500, replace=False)
+    assert np.array_equal(oracle.decode_rows(s, sample, L), rows[sample])
+    with ibp.ibp_open(s, 0, ibp.IBP_OPEN_PAYLOAD_DEVICE) as h:
+        first, count = 5, n - 11
+        say(f"[part deferred] G={G or n} chunk={cs} range ({first}, {count})")
+        out = _out(torch, count, L)
+        ibp.ibp_decompress(h, first, count, out)
+        torch.cuda.synchronize()
+        assert np.array_equal(_rows(out, count, L), rows[first:first + count])
+        assert (out[count * L:].cpu().numpy() == 0xA5).all()
+        rng = np.random.default_rng(6)
+        for order, ids in (("random", rng.integers(0, n, size=n)), ("sorted", np.sort(rng.integers(0, n, size=n)))):
+            say(f"[part deferred] G={G or n} chunk={cs} gather {order} ids={ids.size}")
+            out = _out(torch, ids.size, L)
+            ibp.ibp_gather_decompress_device(h, torch.from_numpy(ids.astype(np.int64)).cuda(), out,
+                                             out_cap=ids.size * L)
+            torch.cuda.synchronize()
+            assert np.array_equal(_rows(out, ids.size, L), rows[ids])
+        assert ibp.ibp_device_errors(h) == 0
+
+
 @pytest.mark.timeout(600)
 def test_participation_gnn_gather_full(torch):
     """The 2.4M x 100 fp32 GNN features under one global Mask at T = 0.8 n (8-byte
