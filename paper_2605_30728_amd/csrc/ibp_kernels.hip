@@ -391,6 +391,12 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
     if constexpr (!STAGED) off_l = s.index[g_l];
     const uint32_t off_lo = (uint32_t)off_l, off_hi = (uint32_t)(off_l >> 32);
     const uint64_t bad = __ballot(l < cnt && !valid);
+    const uint64_t okm = __ballot(l < cnt && valid);   // requests whose rows are stored
+    // requests whose cluster is the previous request's (sorted ids put them together)
+    const uint32_t prev = (l ? l - 1u : 0u) * 4u;
+    const uint32_t pg_lo = (uint32_t)__builtin_amdgcn_ds_bpermute((int)prev, (int)g_lo);
+    const uint32_t pg_hi = (uint32_t)__builtin_amdgcn_ds_bpermute((int)prev, (int)g_hi);
+    const uint64_t samep = __ballot(l > 0 && pg_lo == g_lo && pg_hi == g_hi);
     uint32_t *__restrict__ out_seg = out + i0 * W;
     if (bad) {
         for (uint32_t i = 0; i < cnt; ++i)
@@ -416,8 +422,8 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
             const uint32_t i = pbase + u;
-            const bool row_ok = i < cnt && !((bad >> (i & 63)) & 1ull);
-            uint32_t *__restrict__ orow = out_seg + (uint64_t)slot_of(i) * W;
+            const bool row_ok = (okm >> (i & 63)) & 1ull;
+            uint32_t *__restrict__ orow = out_seg + (uint64_t)i * W;
 #pragma unroll
             for (int j = 0; j < K; ++j) {
                 const uint32_t w = l + kWave * j;
@@ -445,8 +451,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
             const int up = u > 0 ? u - 1 : 0;
             const uint32_t i = slot_of(base_i + u);
             // sorted ids put rows of one cluster next to each other: a row whose cluster
-            // is its predecessor's reuses that row's offsets and hole count (uniform branch)
-            const bool same = u > 0 && rd64(g_lo, g_hi, i) == rd64(g_lo, g_hi, slot_of(base_i + up));
+            // is its predecessor's reuses that row's offsets and hole count (uniform branch;
+            // slots past the end repeat the last request, so they always do)
+            const bool same = u > 0 && (base_i + u >= cnt || ((samep >> ((base_i + u) & 63)) & 1ull));
             if (same) {
 #pragma unroll
                 for (int j = 0; j < K; ++j) {
