@@ -1012,20 +1012,24 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
         }
         return hipGetLastError();
     }
-    // rows of several tiles: one row at a time per wave
-    const uint32_t per_wave = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(16, n / 16384));
-    const uint64_t waves = (n + per_wave - 1) / per_wave;
-    const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
-    if (ids)
-        hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcIds>), grid, block, 0, stream, s, p, pay_base, ids, sg, soff,
-                           first, n, o, per_wave, err);
-    else if (sg)
-        hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcStaged>), grid, block, 0, stream, s, p, pay_base, ids, sg,
-                           soff, first, n, o, per_wave, err);
-    else
-        hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcRange>), grid, block, 0, stream, s, p, pay_base, ids, sg,
-                           soff, first, n, o, per_wave, err);
-    return hipGetLastError();
+    // rows of several tiles (only at eight words per lane): one row at a time per wave
+    if constexpr (K == 8) {
+        const uint32_t per_wave = (uint32_t)std::max<uint64_t>(1, std::min<uint64_t>(16, n / 16384));
+        const uint64_t waves = (n + per_wave - 1) / per_wave;
+        const dim3 grid((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock)), block(kBlock);
+        if (ids)
+            hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcIds>), grid, block, 0, stream, s, p, pay_base, ids, sg, soff,
+                               first, n, o, per_wave, err);
+        else if (sg)
+            hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcStaged>), grid, block, 0, stream, s, p, pay_base, ids, sg,
+                               soff, first, n, o, per_wave, err);
+        else
+            hipLaunchKernelGGL((k_part_rows<K, MAXR, kSrcRange>), grid, block, 0, stream, s, p, pay_base, ids, sg,
+                               soff, first, n, o, per_wave, err);
+        return hipGetLastError();
+    } else {
+        return hipErrorInvalidValue;
+    }
 }
 
 

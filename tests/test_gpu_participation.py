@@ -15,14 +15,16 @@ FLAGS = {"device": ibp.IBP_OPEN_PAYLOAD_DEVICE, "host": ibp.IBP_OPEN_PAYLOAD_HOS
 
 # (kind, n_rows, row_bytes, group_rows, chunk_bytes, threshold, sample_every): chunk sizes
 # of 1-4 words, thresholds from 0.55 to 1, global and per-cluster masks, sampled masks,
-# rows needing several tiles (W > 512), rows stored raw, clusters of one row
+# rows needing several tiles (W > 512) under one global and per-cluster masks, rows stored
+# raw, clusters of one row
 PCASES = [("floats", 300, 400, 32, 4, (4, 5), 1), ("floats", 300, 400, 1000, 8, (4, 5), 1),
           ("sparse", 129, 256, 32, 8, (3, 4), 2), ("random", 97, 12, 5, 4, (9, 10), 1),
           ("specials", 70, 16, 7, 8, (7, 10), 3), ("onebit", 50, 36, 10, 12, (5, 6), 1),
           ("alternating", 80, 24, 8, 4, (2, 3), 1), ("floats", 150, 2400, 700, 8, (4, 5), 4),
           ("random", 40, 64, 40, 4, (11, 20), 1), ("floats", 70, 4096, 100, 16, (4, 5), 1),
           ("sparse", 200, 512, 1, 16, (4, 5), 1), ("floats", 333, 256, 64, 4, (1, 1), 1),
-          ("smallint", 65, 128, 1000, 4, (3, 5), 1)]
+          ("smallint", 65, 128, 1000, 4, (3, 5), 1), ("floats", 90, 2400, 16, 8, (4, 5), 1),
+          ("specials", 60, 3000, 1000, 12, (7, 10), 1)]
 IDS = [f"{c[0]}-{c[1]}x{c[2]}-G{c[3]}-C{c[4]}-T{c[5][0]}of{c[5][1]}-s{c[6]}" for c in PCASES]
 
 
