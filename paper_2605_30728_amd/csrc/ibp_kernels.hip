@@ -661,13 +661,13 @@ __global__ __launch_bounds__(kBlock) void k_part_rows(DevStream s, const uint32_
 // RB participation-scheme rows of one cluster (tile t), one tile each (W <= 64K), in two
 // stages. part_batch_load: the participation bits of all RB rows (loaded together, or
 // prefetched with the lookup), then every row's widths, scan and two-dword windows.
-// part_batch_rebuild: the rebuilt words. Between the two the caller stores the previous
-// batch, so those stores leave after this batch's window loads and the compiler never
-// waits for them before reusing registers. Loads are unconditional with clamped addresses
+// part_batch_rebuild: the rebuilt words. With deferred stores the caller stores the
+// previous batch between the two, so those stores leave after this batch's window loads
+// and the compiler never waits for them before reusing registers. Loads are unconditional with clamped addresses
 // (inside the row or the readable slack), so no exec-masked load makes earlier loads drain.
 //
 // Everything a batch knows about its rows is wave-uniform and read on demand from the
-// lanes of the lookup (lane i holds item i): a row's byte offset and prefetched
+// lanes of the lookup (lane i holds item i): a row's first data bit and prefetched
 // participation dwords by readlane, whether it is raw or to be stored from bit masks. A
 // row's chunk bit becomes an all-ones or all-zeros lane mask (a sign-extended bit-field
 // extract), which then selects the word's width and its rebuilt or raw value by bitfield
@@ -785,17 +785,6 @@ __device__ __forceinline__ void part_store(PartPending<RB, K> &pp, uint32_t *__r
         }
     }
     pp.ok = 0;
-}
-
-// Store what is pending and drop the words: on paths that set up a tile or decode row by
-// row, the words are then not kept live (the compiler cannot tell that `ok` is zero).
-template <int RB, int K>
-__device__ __forceinline__ void part_flush(PartPending<RB, K> &pp, uint32_t *__restrict__ out_seg, uint32_t W) {
-    part_store(pp, out_seg, W);
-#pragma unroll
-    for (int u = 0; u < RB; ++u)
-#pragma unroll
-        for (int j = 0; j < K; ++j) pp.v[u][j] = 0u;
 }
 
 // One batch: its loads, then (DEFER) the previous batch's stores, its rebuild, and
@@ -933,14 +922,14 @@ __global__ __launch_bounds__(kBlock, (ONE && (K == 1 || (K == 2 && PRE != 0))) ?
         const uint64_t tail = RB > 1 ? kTail << (i + 1) : 0ull;   // i + RB <= seg <= 64
         if ((samep & tail) == tail) {
             if (g0 != cached_g) {
-                part_flush(pend, out_seg, W);
+                part_store(pend, out_seg, W);
                 tile_setup(t, s.meta + g0 * 2ull * W, W, 0, 0);
                 cached_g = g0;
             }
             part_batch_step_any<RB, PRE, DEFER>(t, pay32, bit_l, pdw, i, cnt - 1, rawm, ok, m, C, W, full,
                                                 out_seg, pend);
         } else {
-            part_flush(pend, out_seg, W);
+            part_store(pend, out_seg, W);
 #pragma unroll
             for (int u = 0; u < RB; ++u) {
                 if (!((ok >> u) & 1u)) continue;
