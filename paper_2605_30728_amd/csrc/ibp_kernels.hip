@@ -991,9 +991,10 @@ hipError_t launch_part_k(const DevStream &s, const uint32_t *p, uint64_t pay_bas
             else if (pre == 2) go(std::integral_constant<int, 2>{}, defer_tag);
             else if constexpr (K > 1) go(std::integral_constant<int, 0>{}, defer_tag);   // K = 1: at most 64 chunks
         };
-        // deferred stores pay at one word per lane; wider rows need the registers more
-        // (measured: 4% faster at K = 1, 15% slower at K = 2)
-        if constexpr (K == 1) {
+        // deferred stores, measured: the KV layer (K = 1) 4% faster, 1 KB rows read in place
+        // from host memory (K = 4) 5-25% faster; at K = 2 their registers cost a wave per
+        // SIMD and the GNN gather ran 15% slower
+        if constexpr (K != 2) {
             if (nb > 1) go_pre(std::true_type{});
             else go_pre(std::false_type{});
         } else {

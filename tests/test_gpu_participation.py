@@ -122,16 +122,19 @@ def test_participation_library_stream(torch):
         assert np.array_equal(_rows(out, 5000, 400), rows)
 
 
+DEFERRED = [(256, 270_000, 32, 4), (256, 270_000, 32, 8), (256, 270_000, 0, 8), (1024, 70_000, 0, 8),
+            (1024, 70_000, 32, 16), (2048, 40_000, 0, 8), (2048, 40_000, 32, 8)]
+
+
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("G,cs", [(32, 4), (32, 8), (0, 8)], ids=["G32-C4", "G32-C8", "global-C8"])
-def test_participation_deferred_batches(torch, G, cs):
-    """Rows of one word per lane (256 B) in launches large enough for several batches per
-    wave (deferred stores): per-cluster Masks, where batches straddle clusters and decode
-    row by row, and one global Mask; 64 and 32 chunks per row (two and one participation
-    dwords fetched with the lookup). Range decode from an unaligned first row with a ragged
+@pytest.mark.parametrize("L,n,G,cs", DEFERRED, ids=[f"{c[0]}B-G{c[2] or 'all'}-C{c[3]}" for c in DEFERRED])
+def test_participation_deferred_batches(torch, L, n, G, cs):
+    """Launches large enough for two batches per wave (deferred stores) at one, four and
+    eight words per lane: per-cluster Masks, where batches straddle clusters and decode row
+    by row, and one global Mask; 32 to 256 chunks per row (participation dwords fetched with
+    the lookup or loaded per batch). Range decode from an unaligned first row with a ragged
     count, gathers of random and of sorted ids; every row checked against the original rows,
     a sample of the stream against the oracle."""
-    n, L = 270_000, 256
     rows = structured_rows("floats", n, L, seed=77)
     s = ibp.ibp_compress_ex(rows, G or n, cs, (4, 5), 1)
     sample = np.random.default_rng(5).choice(n, 500, replace=False)
