@@ -94,7 +94,10 @@ def kernel_name(workload, W, part=False):
     k = wk_for(W)
     if part:
         maxr = {1: 4, 2: 4, 4: 2, 8: 1}[k]
-        return f"k_part_rows<{k},{maxr},{'ids' if workload in GATHERS else 'range'}>"
+        src = 'ids' if workload in GATHERS else 'range'
+        if W <= 512:
+            return f"k_part_batched<{k},{maxr},{ {1: 8, 2: 4, 4: 2, 8: 1}[k] },{src}>"
+        return f"k_part_rows<{k},{maxr},{src}>"
     if workload in GATHERS:
         rb = {1: 8, 2: 4, 4: 2, 8: 1}[k]
         return f"k_gather_rows<{k},{rb}>" if W <= 512 else "k_gather_tiled"
@@ -104,7 +107,7 @@ def kernel_name(workload, W, part=False):
 def measured_traffic(workload, part=False):
     """HBM bytes per launch from the committed rocprofv3 counter summary of this workload,
     or None when the kernel source has changed since the counters were taken."""
-    kind = "k_part_rows" if part else "k_gather_rows" if workload in GATHERS else "k_decompress"
+    kind = "k_part_batched" if part else "k_gather_rows" if workload in GATHERS else "k_decompress"
     path = os.path.join(ROOT, "profiles", f"{kind}_{workload}.md")
     if not os.path.exists(path):
         return None
