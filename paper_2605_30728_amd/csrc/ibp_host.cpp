@@ -445,17 +445,49 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
     } catch (const std::bad_alloc &) {
         return fail(IBP_ENOMEM, "host allocation for metadata failed");
     }
+    // Adds, for every bit position of the row, how many of the counted rows r0, r0 + every,
+    // ... (< r1) have that bit set. The counts are kept bit-sliced while rows stream in:
+    // plane k holds bit k of every counter (one u32 of 32 counters per word), so adding a
+    // row is a ripple-carry add of its words into the planes, word-parallel (and vectorised
+    // over the words) instead of an increment per set bit; the carry usually dies within a
+    // few planes. The planes are flushed into cnt every 255 rows, before an 8-bit count can
+    // overflow.
     auto count_rows = [&](const uint8_t *grp, uint64_t r0, uint64_t r1, uint64_t *cnt) {
-        for (uint64_t r = r0; r < r1; r += every) {
-            const uint8_t *row = grp + r * L;
-            for (uint32_t w = 0; w < W; ++w) {
-                uint32_t x = load_u32(row + 4 * w);
-                while (x) {
-                    ++cnt[32ull * w + (uint32_t)__builtin_ctz(x)];
-                    x &= x - 1;
+        // local copies: the planes are u32 stores, which the compiler cannot otherwise prove
+        // leave the captured sizes alone (it would reload them and not vectorise)
+        const uint32_t nw = W;
+        const uint64_t row_len = L, step = every;
+        std::vector<uint32_t> planes(8ull * nw, 0u), carry(nw);
+        uint32_t pending = 0;
+        auto flush = [&]() {
+            // counts are at most `pending`, so planes from its bit width up are still zero
+            const uint32_t kmax = 32u - (uint32_t)__builtin_clz(pending);
+            for (uint32_t w = 0; w < nw; ++w)
+                for (uint32_t b = 0; b < 32; ++b) {
+                    uint64_t c = 0;
+                    for (uint32_t k = 0; k < kmax; ++k) c |= (uint64_t)((planes[(uint64_t)k * nw + w] >> b) & 1u) << k;
+                    cnt[32ull * w + b] += c;
                 }
+            std::fill(planes.begin(), planes.end(), 0u);
+            pending = 0;
+        };
+        uint32_t *cy = carry.data();
+        for (uint64_t r = r0; r < r1; r += step) {
+            const uint8_t *row = grp + r * row_len;
+            for (uint32_t w = 0; w < nw; ++w) cy[w] = load_u32(row + 4 * w);
+            for (uint32_t k = 0; k < 8; ++k) {
+                uint32_t *pl = &planes[(uint64_t)k * nw], any = 0;
+                for (uint32_t w = 0; w < nw; ++w) {
+                    const uint32_t t = pl[w] & cy[w];
+                    pl[w] ^= cy[w];
+                    cy[w] = t;
+                    any |= t;
+                }
+                if (!any) break;
             }
+            if (++pending == 255) flush();
         }
+        if (pending) flush();
     };
     auto finish_masks = [&](uint64_t g, const uint64_t *cnt) {
         const uint64_t n = (rows_of(g) + every - 1) / every;
