@@ -19,7 +19,7 @@ KINDS = ["random", "identical", "zeros", "ones", "onebit", "alternating", "float
          "smallint"]
 PLACEMENTS = [ibp.IBP_OPEN_PAYLOAD_DEVICE, ibp.IBP_OPEN_PAYLOAD_HOST, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY,
               ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED]
-N_CASES = 160
+N_CASES = 600
 
 
 def say(*a):
