@@ -825,6 +825,94 @@ __device__ __forceinline__ void part_batch_step_any(const Tile<K, MAXR> &t, cons
 #undef IBP_PART_STEP
 }
 
+// RB participation-scheme rows of a batch whose rows lie in different clusters (a gather
+// under per-cluster Masks). Every row's Mask/Bitval words are loaded together, then each row
+// takes the same widths, scan and windows as a batch of one cluster, and its compressed
+// words are rebuilt with the holes deposit: a setup of runs per row would cost more than it
+// saves. Stores are immediate (this path keeps no words pending).
+template <int RB, int PRE, int K>
+__device__ __forceinline__ void part_mixed_batch(const DevStream &s, const uint32_t *__restrict__ pay32,
+                                                 uint64_t g_l, uint64_t bit_l, const uint32_t (&pdw)[2],
+                                                 uint32_t i, uint32_t last, uint64_t rawm, uint32_t ok, uint32_t m,
+                                                 uint32_t C, uint32_t W, const uint32_t (&full)[K],
+                                                 uint32_t *__restrict__ out_seg) {
+    const uint32_t l = lane_id();
+    uint32_t nm[RB][K], bv[RB][K];
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+        const uint32_t *__restrict__ mg = s.meta + lane_u64(g_l, min(i + u, last)) * 2ull * W;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t w = l + kWave * j, wc = w < W ? w : 0u;
+            nm[u][j] = mg[wc];
+            bv[u][j] = mg[W + wc];
+        }
+    }
+    uint32_t pd[RB];
+    if constexpr (PRE == 0) {
+        const uint32_t nd = (((W - 1) / m) >> 5) + 1;
+        const uint32_t ql = min(l, nd - 1);
+#pragma unroll
+        for (int u = 0; u < RB; ++u) {
+            const uint32_t iu = min(i + u, last);
+            const uint32_t raw = (uint32_t)(rawm >> iu) & 1u;
+            const uint64_t pbit = lane_u64(bit_l, iu) - (raw ? 0u : C);
+            const uint32_t *__restrict__ p = pay32 + (pbit >> 5);
+            pd[u] = __builtin_amdgcn_alignbit(p[ql + 1], p[ql], (uint32_t)pbit & 31u) & (raw - 1u);
+        }
+    }
+    uint32_t d0[RB][K], d1[RB][K], bs[RB][K], nh[RB];
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+        const uint32_t iu = min(i + u, last);
+        const uint64_t rbit = lane_u64(bit_l, iu);
+        uint32_t d_lo = 0, d_hi = 0;
+        if constexpr (PRE >= 1) d_lo = (uint32_t)__builtin_amdgcn_readlane((int)pdw[0], (int)iu);
+        if constexpr (PRE >= 2) d_hi = (uint32_t)__builtin_amdgcn_readlane((int)pdw[1], (int)iu);
+        uint32_t width[K], sel[K], runs = 0;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t w = l + kWave * j;
+            const uint32_t c = (w < W ? w : 0u) / m;
+            uint32_t dw;
+            if constexpr (PRE == 0) dw = (uint32_t)__builtin_amdgcn_ds_bpermute((int)(((c >> 5) & 63u) * 4u), (int)pd[u]);
+            else if constexpr (PRE == 1) dw = d_lo;
+            else dw = (c >> 5) ? d_hi : d_lo;
+            sel[j] = (uint32_t)__builtin_amdgcn_sbfe((int)dw, c & 31u, 1u);
+            nm[u][j] = w < W ? ~nm[u][j] : 0u;   // the variant positions
+            bv[u][j] = w < W ? bv[u][j] : 0u;
+            width[j] = bit_select(sel[j], (uint32_t)__builtin_popcount(nm[u][j]), full[j]);
+            runs = max(runs, run_count(nm[u][j]));
+        }
+        const uint32_t *__restrict__ p = pay32 + (rbit >> 5);
+        uint32_t c = (uint32_t)rbit & 31u;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t inc = wave_incl_scan(width[j]);
+            const uint32_t b = c + inc - width[j];
+            if (j + 1 < K) c += (uint32_t)__builtin_amdgcn_readlane((int)inc, 63);
+            d0[u][j] = p[b >> 5];
+            d1[u][j] = p[(b >> 5) + 1];
+            bs[u][j] = bit_select(31u, b, sel[j]);
+        }
+        const uint32_t most = wave_max(runs);
+        nh[u] = most ? most - 1u : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+        if (!((ok >> u) & 1u)) continue;
+        uint32_t *__restrict__ orow = out_seg + (uint64_t)(i + u) * W;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const uint32_t x = __builtin_amdgcn_alignbit(d1[u][j], d0[u][j], bs[u][j]);
+            const uint32_t y = word_deposit(bv[u][j], nm[u][j], x, nh[u]);
+            const uint32_t v = bit_select((uint32_t)((int32_t)bs[u][j] >> 31), y, x);
+            const uint32_t w = l + kWave * j;
+            if (w < W) store_out(&orow[w], v);
+        }
+    }
+}
+
 // Participation-scheme rows that fit one tile (W <= 64K), in batches of RB rows. With
 // DEFER (a wave of several batches) each batch's stores wait until the next batch's
 // window loads have left; one batch per wave stores at once and keeps fewer registers. A wave
@@ -930,18 +1018,12 @@ __global__ __launch_bounds__(kBlock, (ONE && (K == 1 || (K == 2 && PRE != 0))) ?
                                                 out_seg, pend);
         } else {
             part_store(pend, out_seg, W);
+            // in halves: the per-row metadata would otherwise cost this kernel occupancy
+            constexpr int H = RB > 1 ? RB / 2 : 1;
 #pragma unroll
-            for (int u = 0; u < RB; ++u) {
-                if (!((ok >> u) & 1u)) continue;
-                const uint64_t gu = lane_u64(g_l, i + u);
-                if (gu != cached_g) {
-                    tile_setup(t, s.meta + gu * 2ull * W, W, 0, 0);
-                    cached_g = gu;
-                }
-                const bool raw = (rawm >> (i + u)) & 1ull;
-                const uint64_t rbyte = (lane_u64(bit_l, i + u) - (raw ? 0u : C)) >> 3;
-                part_tile_any(t, pay32, rbyte, raw, m, raw ? 0u : C, W, 0, out_seg + (uint64_t)(i + u) * W);
-            }
+            for (int h = 0; h < RB; h += H)
+                part_mixed_batch<H, PRE>(s, pay32, g_l, bit_l, pdw, i + h, cnt - 1, rawm, (ok >> h) & ((1u << H) - 1u),
+                                         m, C, W, full, out_seg);
         }
     }
     part_store(pend, out_seg, W);
