@@ -914,11 +914,12 @@ __device__ __forceinline__ void part_mixed_batch(const DevStream &s, const uint3
 }
 
 // Participation-scheme rows that fit one tile (W <= 64K), in batches of RB rows. With
-// DEFER (a wave of several batches) each batch's stores wait until the next batch's
-// window loads have left; one batch per wave stores at once and keeps fewer registers. A wave
-// owns `seg` (<= 64) work items; lane i < seg first locates item i (its cluster, the
-// byte of its row and its size), then batches of RB rows are decoded with part_batch
-// while they share a cluster (always, under one global Mask), else row by row.
+// DEFER (two batches per wave) each batch's stores wait until the next batch's window
+// loads have left; otherwise a batch stores at once and keeps fewer registers. A wave owns
+// `seg` (<= 64) work items; lane i < seg first locates item i (its cluster, the first data
+// bit of its row and its size). A batch whose rows share a cluster (always under one global
+// Mask, ONE) is decoded with that cluster's tile; a batch of rows from different clusters
+// loads each row's Mask/Bitval words (part_mixed_batch).
 template <int K, int MAXR, int RB, int SRC, int PRE, bool DEFER, bool ONE>
 __global__ __launch_bounds__(kBlock, (ONE && (K == 1 || (K == 2 && PRE != 0))) ? 8 : 1) void k_part_batched(DevStream s, const uint32_t *__restrict__ pay32,
                                                           uint64_t pay_base, const int64_t *__restrict__ ids,
