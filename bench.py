@@ -62,17 +62,21 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2605_30728_amd", "csrc", f)
                   for f in ("ibp_kernels.hip", "ibp_cache_kernels.hip", "ibp_wave.hpp", "ibp_device.hpp")]
 
 
-def kernel_sources_sha256():
-    """sha256 of the kernel sources' code: comments, trailing blanks and empty lines are
+def code_sha256(texts):
+    """sha256 of C/HIP source texts' code: comments, trailing blanks and empty lines are
     dropped first, so that editing a comment does not retire the counters taken on the code."""
     h = hashlib.sha256()
-    for path in KERNEL_SOURCES:
-        text = re.sub(r"/\*.*?\*/", "", open(path).read(), flags=re.S)
+    for text in texts:
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         for line in text.splitlines():
             code = re.sub(r"//.*", "", line).rstrip()
             if code:
                 h.update(code.encode() + b"\n")
     return h.hexdigest()
+
+
+def kernel_sources_sha256():
+    return code_sha256(open(path).read() for path in KERNEL_SOURCES)
 GATHERS = ("gnn_gather", "dlrm", "big_gnn")
 STREAMS = ("kv_bf16", "tiny_gnn")
 DESCRIPTIONS = {

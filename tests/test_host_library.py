@@ -180,3 +180,15 @@ def test_identity_stream_is_valid_and_raw():
     d = ibp.ibp_describe(s)
     assert d["payload_bytes"] == rows.nbytes and d["n_groups"] == 5
     assert np.array_equal(oracle.decompress(s, 70, 64), rows)
+
+
+def test_kernel_code_hash_ignores_comments_only():
+    """The hash that decides whether the stored counter traffic still describes the kernels:
+    comment and blank-line edits keep it, any code edit changes it."""
+    import bench
+    src = "// header\n__global__ void k(int *p) {\n    p[0] = 1;   // store\n}\n"
+    same = "/* a block\n   comment */\n__global__ void k(int *p) {\n\n    p[0] = 1;\n}\n// trailer\n"
+    other = "__global__ void k(int *p) {\n    p[0] = 2;\n}\n"
+    assert bench.code_sha256([src]) == bench.code_sha256([same])
+    assert bench.code_sha256([src]) != bench.code_sha256([other])
+    assert len(bench.kernel_sources_sha256()) == 64
