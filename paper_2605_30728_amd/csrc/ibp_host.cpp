@@ -630,10 +630,18 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
                     nacc -= 32;
                 }
             };
-            for (uint32_t c = 0; c < C; ++c) {
-                ok[c] = chunk_ok(mk, row, c);
-                put(ok[c], 1);
+            // the participation bits, up to 32 per put
+            for (uint32_t c0 = 0; c0 < C; c0 += 32) {
+                const uint32_t nb = std::min<uint32_t>(32, C - c0);
+                uint64_t bits = 0;
+                for (uint32_t c = 0; c < nb; ++c) {
+                    ok[c0 + c] = chunk_ok(mk, row, c0 + c);
+                    bits |= (uint64_t)ok[c0 + c] << c;
+                }
+                put(bits, nb);
             }
+            // then every word: all 32 bits of a raw chunk, or its variant bits gathered run
+            // by run into one field of popcount(~Mask) bits
             for (uint32_t c = 0; c < C; ++c) {
                 for (uint32_t j = 0; j < m; ++j) {
                     const uint32_t w = c * m + j;
@@ -642,8 +650,13 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
                         put(x, 32);
                         continue;
                     }
-                    for (uint32_t q = first[w]; q < first[w + 1]; ++q)
-                        put((x >> runs[q].lo) & ((1ull << runs[q].len) - 1), runs[q].len);
+                    uint64_t packed = 0;
+                    uint32_t width = 0;
+                    for (uint32_t q = first[w]; q < first[w + 1]; ++q) {
+                        packed |= ((x >> runs[q].lo) & ((1ull << runs[q].len) - 1)) << width;
+                        width += runs[q].len;
+                    }
+                    if (width) put(packed, width);
                 }
             }
             for (uint32_t b = 0; b < (nacc + 7) / 8; ++b) dp[b] = (uint8_t)(acc >> (8 * b));
