@@ -242,6 +242,28 @@ ibp_status ibp_gather_decompress_device(ibp_handle *h, const int64_t *d_row_ids,
                                         void *stream);
 
 /*
+ * ibp_gather_decompress_noalloc -- as ibp_gather_decompress (host row ids), for callers
+ * that cannot allocate memory during the call: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc. It calls no hipMalloc, hipFree or other
+ * allocating routine: the ids are copied (hipMemcpyAsync on `stream`) into a fixed device
+ * scratch array of the library, 4,194,304 int64 ids (32 MiB) per device, which each
+ * device holds from the first ibp_open on it until the process ends, and the gather
+ * kernel reads them there. For a handle opened with IBP_OPEN_PAYLOAD_DEVICE or
+ * IBP_OPEN_PAYLOAD_HOST_ZERO_COPY[_ALIGNED]. The ids are range-checked on the host first
+ * (nothing is enqueued on IBP_ERANGE). From pageable host memory the HIP runtime has read
+ * row_ids when the call returns; from pinned host memory the copy is asynchronous and
+ * row_ids must stay unchanged until `stream` reaches this call. Every call on a device
+ * shares that device's scratch and leaves its ids there: calls in a row on one stream
+ * are ordered, but calls that overlap on one device (other streams, other threads or
+ * handles) race and may decode each other's ids.
+ * Errors: IBP_EINVAL (null pointers with n_ids > 0, n_ids above 4,194,304, or a handle
+ * opened with IBP_OPEN_PAYLOAD_HOST), IBP_ERANGE, IBP_ENOMEM (out_cap too small),
+ * IBP_EHIP, IBP_ESTATE.
+ */
+ibp_status ibp_gather_decompress_noalloc(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids,
+                                         void *d_out, uint64_t out_cap, void *stream);
+
+/*
  * ibp_device_errors -- synchronize the device and return (in *count) how many
  * out-of-range device ids the gather kernels met since ibp_open or the last call of
  * this function, then reset the counter.

@@ -80,6 +80,7 @@ _SIGS = {
     "ibp_decompress": [_vp, _u64, _u64, _vp, _u64, _vp],
     "ibp_gather_decompress": [_vp, _vp, _u64, _vp, _u64, _vp],
     "ibp_gather_decompress_device": [_vp, _vp, _u64, _vp, _u64, _vp],
+    "ibp_gather_decompress_noalloc": [_vp, _vp, _u64, _vp, _u64, _vp],
     "ibp_device_errors": [_vp, ctypes.POINTER(_u64)],
     "ibp_get_desc": [_vp, ctypes.POINTER(ibp_desc)],
     "ibp_get_stats": [_vp, ctypes.POINTER(ibp_stats)],
@@ -249,6 +250,13 @@ def ibp_gather_decompress(h, row_ids, d_out, out_cap=None, stream=None):
     cap = _nbytes(d_out) if out_cap is None else out_cap
     _check(lib().ibp_gather_decompress(h.ptr, ids.ctypes.data, ids.size, _ptr(d_out), cap, _stream(stream)),
            "ibp_gather_decompress")
+
+
+def ibp_gather_decompress_noalloc(h, row_ids, d_out, out_cap=None, stream=None):
+    ids = np.ascontiguousarray(row_ids, dtype=np.int64)
+    cap = _nbytes(d_out) if out_cap is None else out_cap
+    _check(lib().ibp_gather_decompress_noalloc(h.ptr, ids.ctypes.data, ids.size, _ptr(d_out), cap,
+                                               _stream(stream)), "ibp_gather_decompress_noalloc")
 
 
 def ibp_gather_decompress_device(h, d_row_ids, d_out, n_ids=None, out_cap=None, stream=None):

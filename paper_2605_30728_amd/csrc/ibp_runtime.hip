@@ -77,6 +77,42 @@ hipError_t wait_event(hipEvent_t e) {
 }  // namespace
 }  // namespace ibp
 
+// Fixed device scratch of the allocation-free host-id gather: the row ids of one call are
+// copied here and the gather kernel reads them from here. One copy per device, held until
+// the process ends; every call on a device shares it (calls that overlap on one device
+// race). Host code never uses this name as an address: it uses the per-device pointer
+// that hipGetSymbolAddress returns (scratch_on_device).
+constexpr uint64_t kScratchIds = 4ull << 20;   // 4,194,304 ids = 32 MiB
+static __device__ __align__(256) int64_t scratch[kScratchIds];
+
+namespace ibp {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int64_t *g_scratch_ptr[kMaxDevices] = {};
+hipError_t g_scratch_err[kMaxDevices] = {};
+bool g_scratch_done[kMaxDevices] = {};
+
+// Device address of `scratch` on `device`, resolved once per device with that device
+// current (each device holds its own copy of the array at its own address).
+hipError_t scratch_on_device(int device, int64_t **ptr) {
+    *ptr = nullptr;
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_done[device]) {
+        void *p = nullptr;
+        g_scratch_err[device] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_ptr[device] = g_scratch_err[device] == hipSuccess ? static_cast<int64_t *>(p) : nullptr;
+        g_scratch_done[device] = true;
+    }
+    *ptr = g_scratch_ptr[device];
+    return g_scratch_err[device];
+}
+
+}  // namespace
+}  // namespace ibp
+
 using namespace ibp;
 
 struct ibp_handle {
@@ -90,6 +126,8 @@ struct ibp_handle {
     uint8_t *d_payload = nullptr;
     const uint8_t *k_payload = nullptr;   // what the kernels read: d_payload or the pinned host payload
     unsigned long long *d_err = nullptr;
+    int64_t *scratch_ids = nullptr;       // this device's `scratch` (allocation-free gather)
+    hipError_t scratch_err = hipSuccess;
     // host ids of gathers over a device or zero-copy payload: two slots alternate, so the
     // ids of call k+1 are staged while the kernel of call k still reads slot k%2
     int64_t *h_ids[kIdSlots] = {}, *d_ids[kIdSlots] = {};
@@ -461,6 +499,8 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     int prev = 0;
     ignore(hipGetDevice(&prev));
     if (hipSetDevice(device) != hipSuccess) return fail(IBP_EHIP, "hipSetDevice failed");
+    int64_t *scratch_ids = nullptr;
+    const hipError_t scratch_err = scratch_on_device(device, &scratch_ids);
 
     ibp_handle *h = new (std::nothrow) ibp_handle();
     if (!h) {
@@ -469,6 +509,8 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     }
     h->device = device;
     h->flags = flags;
+    h->scratch_ids = scratch_ids;
+    h->scratch_err = scratch_err;
     h->d = d;
     h->pool = new Pool(std::min(16, online_cpus()));
     auto bail = [&](ibp_status s) {
@@ -659,6 +701,36 @@ ibp_status ibp_gather_decompress_device(ibp_handle *h, const int64_t *d_row_ids,
     h->stats.calls += 1;
     h->stats.rows_out += n_ids;
     h->stats.out_bytes += n_ids * h->d.row_bytes;
+    return IBP_OK;
+}
+
+ibp_status ibp_gather_decompress_noalloc(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, void *d_out,
+                                         uint64_t out_cap, void *stream) {
+    clear_error();
+    CallScope cs(h);
+    ibp_status st = check_handle(h, cs);
+    if (st != IBP_OK) return st;
+    if (h->flags == IBP_OPEN_PAYLOAD_HOST)
+        return fail(IBP_EINVAL, "the allocation-free gather needs a handle whose kernels read the payload in place "
+                                "(IBP_OPEN_PAYLOAD_DEVICE or IBP_OPEN_PAYLOAD_HOST_ZERO_COPY[_ALIGNED])");
+    if (n_ids == 0) return IBP_OK;
+    if (!row_ids || !d_out) return fail(IBP_EINVAL, "row ids or output is null");
+    if (n_ids > kScratchIds) return fail(IBP_EINVAL, "n_ids exceeds the fixed scratch of 4194304 ids");
+    const ibp_desc &d = h->d;
+    if (out_cap / d.row_bytes < n_ids) return fail(IBP_ENOMEM, "output capacity too small");
+    if (!h->scratch_ids)
+        return fail(IBP_EHIP, std::string("device scratch is not available: ") + hipGetErrorString(h->scratch_err));
+    for (uint64_t i = 0; i < n_ids; ++i)
+        if (row_ids[i] < 0 || (uint64_t)row_ids[i] >= d.n_rows)
+            return fail(IBP_ERANGE, "row id " + std::to_string(row_ids[i]) + " at position " + std::to_string(i) +
+                                        " is outside [0, " + std::to_string(d.n_rows) + ")");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    IBP_HIP(h, hipMemcpyAsync(h->scratch_ids, row_ids, n_ids * 8, hipMemcpyHostToDevice, s));
+    IBP_HIP(h, dev::launch_gather(h->ds, h->k_payload, h->scratch_ids, nullptr, nullptr, n_ids, d_out, h->d_err, s));
+    h->stats.calls += 1;
+    h->stats.rows_out += n_ids;
+    h->stats.out_bytes += n_ids * d.row_bytes;
+    h->stats.h2d_bytes += n_ids * 8;
     return IBP_OK;
 }
 
