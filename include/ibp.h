@@ -60,6 +60,15 @@
 extern "C" {
 #endif
 
+/*
+ * Test hook (every allocating call: ibp_compress, ibp_compress_ex, ibp_open,
+ * ibp_gather_decompress, ibp_cache_create): while the environment variable
+ * IBP_TEST_FAIL_ALLOC holds a number n >= 1, the n-th allocation that one such call makes
+ * (host, pinned or device, counted from 1 within the call) fails as if memory were
+ * exhausted. The call then returns IBP_ENOMEM, has written nothing to its outputs and
+ * holds nothing more than before (ibp_memory_usage).
+ */
+
 typedef enum {
     IBP_OK = 0,
     IBP_EINVAL = 1,    /* a bad argument (null pointer, size, alignment, flag) */
@@ -138,8 +147,10 @@ enum {
 };
 
 /*
- * ibp_compress_bound -- an upper bound on the stream size of n_rows rows
- * (every row stored raw plus the header, metadata and index). Host only.
+ * ibp_compress_bound -- an upper bound on the stream size of n_rows rows: the header,
+ * metadata and index plus every row at its raw size, since the Fig. 4 size rule never
+ * stores a row in more than its raw bytes (Sec. 4.2: a row that would save nothing is kept
+ * uncompressed, so the data never grows). Host only.
  * Errors: IBP_EINVAL for a null `bound`, row_bytes not a positive multiple of 4,
  * group_rows == 0, or a size that overflows 64 bits.
  */
@@ -180,7 +191,10 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
                            uint64_t out_cap, uint64_t *out_bytes);
 
 /*
- * ibp_describe -- validate a stream and fill *d. Host only. Validation covers the
+ * ibp_describe -- validate a stream and fill *d. The sections mean what Sec. 4.1-4.2 and
+ * Sec. 6.5 define (per-cluster Mask/Bitval, packed rows, the size rule); the container
+ * around them is this library's (the paper prints none), as laid out above. Host only.
+ * Validation covers the
  * header fields, the section offsets, Bitval being zero wherever Mask is zero, a
  * monotone index with off[0] = 0 and off[g+1] - off[g] = n_g * rb_g (clustered
  * scheme) or every row's size agreeing with its participation bits (flags = 1), and
@@ -191,8 +205,11 @@ ibp_status ibp_describe(const void *stream, uint64_t stream_bytes, ibp_desc *d);
 
 /*
  * ibp_open -- validate `stream` (as ibp_describe) and load it for decompression on
- * HIP device `device`: the metadata and index are copied to device memory, and the
- * payload to device memory or to library-owned pinned host memory (see the flags).
+ * HIP device `device`: the metadata and index are copied to device memory once and
+ * serve every later decompression (Sec. 4: the invariant-bit metadata lives in GPU
+ * memory for the whole dataset), and the payload goes to device memory or stays in
+ * library-owned pinned host memory to be read over PCIe on demand (Sec. 5, PCIe transfer
+ * compression; Sec. 4.4), see the flags.
  * The stream buffer is not referenced after ibp_open returns. *h receives a handle
  * owned by the library until ibp_close.
  * Errors: IBP_EINVAL, IBP_ECORRUPT, IBP_ENOMEM, IBP_EHIP.
@@ -266,22 +283,48 @@ ibp_status ibp_gather_decompress_noalloc(ibp_handle *h, const int64_t *row_ids, 
 /*
  * ibp_device_errors -- synchronize the device and return (in *count) how many
  * out-of-range device ids the gather kernels met since ibp_open or the last call of
- * this function, then reset the counter.
+ * this function, then reset the counter. Library plumbing: the paper defines no device
+ * error reporting. An asynchronous failure of an enqueued kernel or copy (a fault, not an
+ * id out of range) is reported by the HIP runtime at the next synchronizing call: this
+ * one (IBP_EHIP, then sticky on the handle), ibp_close, ibp_cache_get_stats, or a
+ * synchronize of the caller's own.
  * Errors: IBP_EINVAL, IBP_EHIP, IBP_ESTATE.
  */
 ibp_status ibp_device_errors(ibp_handle *h, uint64_t *count);
 
-/* ibp_get_desc / ibp_get_stats -- copies of the handle's description and counters. */
+/*
+ * ibp_get_desc / ibp_get_stats / ibp_reset_stats -- a copy of the handle's description,
+ * a copy of its counters, and a reset of the counters. The counters report the bytes the
+ * calls moved host-to-device, which the paper's evaluation normalises by (Sec. 6.1: the
+ * compressed bytes moved over PCIe, as in its no-decode mock system); the calls
+ * themselves are library plumbing. They take the handle like every other call: IBP_ESTATE
+ * while another thread's call runs on it, or once it is closed.
+ * Errors: IBP_EINVAL (null pointers), IBP_ESTATE.
+ */
 ibp_status ibp_get_desc(ibp_handle *h, ibp_desc *d);
 ibp_status ibp_get_stats(ibp_handle *h, ibp_stats *st);
 ibp_status ibp_reset_stats(ibp_handle *h);
 
 /*
- * ibp_close -- wait for the handle's outstanding work, free everything it owns and
- * invalidate it. NULL is accepted (IBP_OK). Closing twice is undefined: the handle
- * memory is freed by the first close. IBP_ESTATE while caches built on it exist.
+ * ibp_close -- wait for the handle's outstanding work, free everything it owns and mark
+ * it closed. Library plumbing (the paper defines no such call). NULL is accepted (IBP_OK).
+ * The handle's small descriptor (well under 1 KiB) stays allocated as a closed marker
+ * until the process ends, so that a second ibp_close, or any other call on the closed
+ * handle, returns IBP_ESTATE and does nothing. IBP_ESTATE also while another thread's
+ * call runs on the handle, or while caches built on it exist (the handle stays open).
+ * IBP_EHIP when outstanding work failed (the handle is closed all the same).
  */
 ibp_status ibp_close(ibp_handle *h);
+
+/*
+ * ibp_memory_usage -- bytes of device memory and of pinned host memory the library
+ * holds right now, over every open handle and cache (metadata, payload copies, staging,
+ * id buffers, cache slabs and tables; not the fixed scratch array of
+ * ibp_gather_decompress_noalloc, which is part of the loaded code object). Library
+ * plumbing for memory accounting and leak checks; the paper defines no such call.
+ * Errors: IBP_EINVAL (null pointers).
+ */
+ibp_status ibp_memory_usage(uint64_t *device_bytes, uint64_t *pinned_bytes);
 
 /*
  * Compressed device-resident row cache (Sec. 5, cache compression). A static set of
@@ -305,7 +348,9 @@ typedef struct {
 
 /*
  * ibp_cache_create -- build a cache holding rows row_ids[0..n_ids) (host memory, read
- * before the call returns; duplicates are held once) of a handle opened with
+ * before the call returns; duplicates are held once), packed back to back in one slab
+ * and mapped by a table of entries as Sec. 5 (cache compression) lays out, of a handle
+ * opened with
  * IBP_OPEN_PAYLOAD_HOST_ZERO_COPY on a clustered-scheme stream (flags = 0) of at most
  * 2048-byte rows. Synchronous. The handle must outlive the cache (ibp_close returns
  * IBP_ESTATE while caches exist).
@@ -317,24 +362,32 @@ ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_id
 /*
  * ibp_cache_gather -- d_out[i] = row(d_row_ids[i]) for i < n_ids (device ids, device
  * output of n_ids * row_bytes bytes) on `stream`; hits are decoded from the slab, misses
- * from host memory. An id out of range gives a zero row and counts in
- * ibp_device_errors() of the handle.
- * Errors: IBP_EINVAL, IBP_ENOMEM (out_cap too small), IBP_EHIP, IBP_ESTATE.
+ * from host memory (Sec. 5: a cache access finds the slab and offset of a tensor and its
+ * compressed flag in the hashmap entry, and decompresses it or reads it). An id out of
+ * range gives a zero row and counts in ibp_device_errors() of the handle.
+ * Errors: IBP_EINVAL, IBP_ENOMEM (out_cap too small), IBP_EHIP, IBP_ESTATE (also on a
+ * destroyed cache).
  */
 ibp_status ibp_cache_gather(ibp_cache *c, const int64_t *d_row_ids, uint64_t n_ids, void *d_out,
                             uint64_t out_cap, void *stream);
 
-/* ibp_cache_get_stats -- synchronize the device and copy the cache's sizes and counters. */
+/* ibp_cache_get_stats -- synchronize the device and copy the cache's sizes and counters
+ * (the hit rate the paper's cache compression raises, Sec. 5). IBP_ESTATE on a destroyed
+ * cache. */
 ibp_status ibp_cache_get_stats(ibp_cache *c, ibp_cache_stats *st);
-/* ibp_cache_reset_stats -- synchronize the device and zero the hit / miss counters. */
+/* ibp_cache_reset_stats -- synchronize the device and zero the hit / miss counters.
+ * IBP_ESTATE on a destroyed cache. */
 ibp_status ibp_cache_reset_stats(ibp_cache *c);
-/* ibp_cache_destroy -- wait for outstanding work and free the cache. NULL is accepted. */
+/* ibp_cache_destroy -- wait for outstanding work and free the cache's device memory.
+ * Library plumbing. NULL is accepted. The cache's small descriptor stays allocated as a
+ * destroyed marker, so a second ibp_cache_destroy (or any call on it) returns IBP_ESTATE. */
 ibp_status ibp_cache_destroy(ibp_cache *c);
 
-/* ibp_last_error -- message of the last failed call on this thread ("" if none). */
+/* ibp_last_error -- message of the last failed call on this thread ("" if none).
+ * Library plumbing (the paper defines no error reporting). */
 const char *ibp_last_error(void);
 
-/* ibp_version -- library/stream format version string. */
+/* ibp_version -- library/stream format version string. Library plumbing. */
 const char *ibp_version(void);
 
 #ifdef __cplusplus

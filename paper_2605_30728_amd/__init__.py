@@ -86,6 +86,7 @@ _SIGS = {
     "ibp_get_stats": [_vp, ctypes.POINTER(ibp_stats)],
     "ibp_reset_stats": [_vp],
     "ibp_close": [_vp],
+    "ibp_memory_usage": [ctypes.POINTER(_u64), ctypes.POINTER(_u64)],
     "ibp_cache_create": [_vp, _vp, _u64, ctypes.POINTER(_vp)],
     "ibp_cache_gather": [_vp, _vp, _u64, _vp, _u64, _vp],
     "ibp_cache_get_stats": [_vp, ctypes.POINTER(ibp_cache_stats)],
@@ -135,6 +136,26 @@ def _ptr(x):
     if isinstance(x, np.ndarray):
         return x.ctypes.data
     raise TypeError(f"cannot take the address of {type(x)}")
+
+
+def _device_tensor(x, what, dtype=None):
+    """Checks that a device argument is a contiguous GPU tensor (of `dtype`, if given)
+    before its address reaches a kernel; an integer is taken as a raw device address."""
+    if isinstance(x, int):
+        return
+    if isinstance(x, np.ndarray) or not hasattr(x, "is_cuda"):
+        raise TypeError(f"{what} must be a GPU tensor (or a raw device address), not {type(x).__name__}")
+    if not x.is_cuda:
+        raise TypeError(f"{what} must be on the GPU, not on {x.device}")
+    if not x.is_contiguous():
+        raise TypeError(f"{what} must be contiguous")
+    if dtype is not None and x.dtype != dtype:
+        raise TypeError(f"{what} must be {dtype}, not {x.dtype}")
+
+
+def _device_ids(x):
+    import torch
+    _device_tensor(x, "row ids", torch.int64)
 
 
 def _nbytes(x):
@@ -241,12 +262,14 @@ def ibp_open(stream, device=0, flags=IBP_OPEN_PAYLOAD_DEVICE):
 
 
 def ibp_decompress(h, first_row, n_rows, d_out, out_cap=None, stream=None):
+    _device_tensor(d_out, "d_out")
     cap = _nbytes(d_out) if out_cap is None else out_cap
     _check(lib().ibp_decompress(h.ptr, first_row, n_rows, _ptr(d_out), cap, _stream(stream)), "ibp_decompress")
 
 
 def ibp_gather_decompress(h, row_ids, d_out, out_cap=None, stream=None):
     ids = np.ascontiguousarray(row_ids, dtype=np.int64)
+    _device_tensor(d_out, "d_out")
     cap = _nbytes(d_out) if out_cap is None else out_cap
     _check(lib().ibp_gather_decompress(h.ptr, ids.ctypes.data, ids.size, _ptr(d_out), cap, _stream(stream)),
            "ibp_gather_decompress")
@@ -254,12 +277,15 @@ def ibp_gather_decompress(h, row_ids, d_out, out_cap=None, stream=None):
 
 def ibp_gather_decompress_noalloc(h, row_ids, d_out, out_cap=None, stream=None):
     ids = np.ascontiguousarray(row_ids, dtype=np.int64)
+    _device_tensor(d_out, "d_out")
     cap = _nbytes(d_out) if out_cap is None else out_cap
     _check(lib().ibp_gather_decompress_noalloc(h.ptr, ids.ctypes.data, ids.size, _ptr(d_out), cap,
                                                _stream(stream)), "ibp_gather_decompress_noalloc")
 
 
 def ibp_gather_decompress_device(h, d_row_ids, d_out, n_ids=None, out_cap=None, stream=None):
+    _device_ids(d_row_ids)
+    _device_tensor(d_out, "d_out")
     n = d_row_ids.numel() if n_ids is None else n_ids
     cap = _nbytes(d_out) if out_cap is None else out_cap
     _check(lib().ibp_gather_decompress_device(h.ptr, _ptr(d_row_ids), n, _ptr(d_out), cap, _stream(stream)),
@@ -270,6 +296,13 @@ def ibp_device_errors(h):
     c = _u64(0)
     _check(lib().ibp_device_errors(h.ptr, ctypes.byref(c)), "ibp_device_errors")
     return c.value
+
+
+def ibp_memory_usage():
+    """(device bytes, pinned host bytes) the library holds over all handles and caches."""
+    dev, pin = _u64(0), _u64(0)
+    _check(lib().ibp_memory_usage(ctypes.byref(dev), ctypes.byref(pin)), "ibp_memory_usage")
+    return dev.value, pin.value
 
 
 def ibp_get_desc(h):
@@ -319,6 +352,8 @@ def ibp_cache_create(h, row_ids):
 
 
 def ibp_cache_gather(c, d_row_ids, d_out, n_ids=None, out_cap=None, stream=None):
+    _device_ids(d_row_ids)
+    _device_tensor(d_out, "d_out")
     n = d_row_ids.numel() if n_ids is None else n_ids
     cap = _nbytes(d_out) if out_cap is None else out_cap
     _check(lib().ibp_cache_gather(c.ptr, _ptr(d_row_ids), n, _ptr(d_out), cap, _stream(stream)), "ibp_cache_gather")

@@ -17,6 +17,7 @@
 // bits, so packing a word costs one shift-and-mask per run.
 #include <algorithm>
 #include <atomic>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <thread>
@@ -30,6 +31,8 @@ namespace ibp {
 
 namespace {
 thread_local std::string g_last_error;
+thread_local int g_alloc_depth = 0;          // nested AllocTestScopes on this thread
+thread_local long long g_alloc_countdown = 0; // allocations left before the injected failure
 
 inline uint32_t load_u32(const uint8_t *p) {
     uint32_t v;
@@ -95,6 +98,23 @@ inline int variant_runs(uint32_t mask, Run *runs) {
 }
 
 }  // namespace
+
+AllocTestScope::AllocTestScope() : outer_(g_alloc_depth++ == 0) {
+    if (!outer_) return;
+    const char *e = std::getenv("IBP_TEST_FAIL_ALLOC");
+    g_alloc_countdown = e ? std::atoll(e) : 0;
+}
+
+AllocTestScope::~AllocTestScope() {
+    --g_alloc_depth;
+    if (outer_) g_alloc_countdown = 0;
+}
+
+bool alloc_fails() { return g_alloc_countdown > 0 && --g_alloc_countdown == 0; }
+
+void check_alloc() {
+    if (alloc_fails()) throw std::bad_alloc();
+}
 
 ibp_status fail(ibp_status s, const std::string &msg) {
     g_last_error = msg;
@@ -286,9 +306,12 @@ ibp_status ibp_compress_bound(uint64_t n_rows, uint32_t row_bytes, uint32_t grou
     return IBP_OK;
 }
 
-ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes, uint32_t group_rows,
-                        int n_threads, void *out, uint64_t out_cap, uint64_t *out_bytes) {
-    clear_error();
+}  // extern "C"
+
+namespace {
+
+ibp_status compress_clustered(const void *rows, uint64_t n_rows, uint32_t row_bytes, uint32_t group_rows,
+                              int n_threads, void *out, uint64_t out_cap, uint64_t *out_bytes) {
     if (!out_bytes) return fail(IBP_EINVAL, "out_bytes is null");
     uint64_t bound;
     ibp_status st = ibp_compress_bound(n_rows, row_bytes, group_rows, &bound);
@@ -305,6 +328,7 @@ ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes, u
     std::vector<uint32_t> meta;
     std::vector<uint64_t> rb;
     try {
+        check_alloc();
         meta.resize(ng * 2ull * W);
         rb.resize(ng);
     } catch (const std::bad_alloc &) {
@@ -344,6 +368,9 @@ ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes, u
     if (total > out_cap) return fail(IBP_ENOMEM, "output capacity smaller than the stream");
     if (!out) return fail(IBP_EINVAL, "out is null");
     uint8_t *dst = static_cast<uint8_t *>(out);
+    // allocated before the first byte of the output is written, so a failure writes nothing
+    check_alloc();
+    std::vector<uint64_t> off(ng + 1);
 
     std::memset(dst, 0, kHeaderBytes);
     std::memcpy(dst, kMagic, 4);
@@ -356,7 +383,6 @@ ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes, u
     store_u64(dst + 48, index_off);
     store_u64(dst + 56, payload_off);
     if (ng) std::memcpy(dst + meta_off, meta.data(), ng * 2ull * L);
-    std::vector<uint64_t> off(ng + 1);
     off[0] = 0;
     for (uint64_t g = 0; g < ng; ++g) off[g + 1] = off[g] + rows_of(g) * rb[g];
     for (uint64_t g = 0; g <= ng; ++g) store_u64(dst + index_off + 8 * g, off[g]);
@@ -403,9 +429,8 @@ ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes, u
     return IBP_OK;
 }
 
-ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes, const ibp_params *p,
-                           int n_threads, void *out, uint64_t out_cap, uint64_t *out_bytes) {
-    clear_error();
+ibp_status compress_participation(const void *rows, uint64_t n_rows, uint32_t row_bytes, const ibp_params *p,
+                                  int n_threads, void *out, uint64_t out_cap, uint64_t *out_bytes) {
     if (!p) return fail(IBP_EINVAL, "params is null");
     if (!out_bytes) return fail(IBP_EINVAL, "out_bytes is null");
     if (p->threshold_den == 0 || p->threshold_num > p->threshold_den ||
@@ -415,7 +440,7 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
     if (p->chunk_bytes == 0) {
         if (p->threshold_num != p->threshold_den || p->sample_every != 1)
             return fail(IBP_EINVAL, "a threshold below 1 or a sampled Mask needs participation bits");
-        return ibp_compress(rows, n_rows, row_bytes, p->group_rows, n_threads, out, out_cap, out_bytes);
+        return compress_clustered(rows, n_rows, row_bytes, p->group_rows, n_threads, out, out_cap, out_bytes);
     }
     if (row_bytes == 0 || row_bytes % 4 != 0)
         return fail(IBP_EINVAL, "row_bytes must be a positive multiple of 4");
@@ -440,6 +465,7 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
     std::vector<uint32_t> meta;
     std::vector<uint32_t> size;
     try {
+        check_alloc();
         meta.resize(ng * 2ull * W);
         size.resize(n_rows);
     } catch (const std::bad_alloc &) {
@@ -517,6 +543,7 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
         });
     } else {
         // few, large clusters (a global Mask): split each cluster's counted rows
+        check_alloc();
         std::vector<uint64_t> part_cnt((size_t)threads * 32ull * W);
         for (uint64_t g = 0; g < ng; ++g) {
             const uint64_t n = rows_of(g), counted = (n + every - 1) / every;
@@ -663,6 +690,28 @@ ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes
         }
     });
     return IBP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ibp_status ibp_compress(const void *rows, uint64_t n_rows, uint32_t row_bytes, uint32_t group_rows,
+                        int n_threads, void *out, uint64_t out_cap, uint64_t *out_bytes) {
+    clear_error();
+    AllocTestScope scope;
+    return guarded([&] {
+        return compress_clustered(rows, n_rows, row_bytes, group_rows, n_threads, out, out_cap, out_bytes);
+    });
+}
+
+ibp_status ibp_compress_ex(const void *rows, uint64_t n_rows, uint32_t row_bytes, const ibp_params *p,
+                           int n_threads, void *out, uint64_t out_cap, uint64_t *out_bytes) {
+    clear_error();
+    AllocTestScope scope;
+    return guarded([&] {
+        return compress_participation(rows, n_rows, row_bytes, p, n_threads, out, out_cap, out_bytes);
+    });
 }
 
 ibp_status ibp_describe(const void *stream, uint64_t stream_bytes, ibp_desc *d) {

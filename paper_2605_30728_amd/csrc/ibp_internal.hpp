@@ -3,7 +3,9 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <exception>
 #include <functional>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -29,6 +31,38 @@ struct StreamView {
 // Thread-local error message plumbing.
 ibp_status fail(ibp_status s, const std::string &msg);
 void clear_error();
+
+// Runs an entry point's body and turns a C++ exception into a status, so that none crosses
+// the C ABI: std::bad_alloc is IBP_ENOMEM, anything else IBP_EINVAL.
+template <class F>
+ibp_status guarded(F &&body) noexcept {
+    try {
+        return body();
+    } catch (const std::bad_alloc &) {
+        return fail(IBP_ENOMEM, "host allocation failed");
+    } catch (const std::exception &e) {
+        return fail(IBP_EINVAL, e.what());
+    } catch (...) {
+        return fail(IBP_EINVAL, "unexpected error");
+    }
+}
+
+// Test hook for allocation failures: while the environment variable IBP_TEST_FAIL_ALLOC
+// holds a number n >= 1, the n-th allocation made by one call of an allocating entry point
+// (counted from 1 within that call) fails as if memory were exhausted. An AllocTestScope
+// at the top of the entry point reads the variable; nested scopes keep the outer count.
+class AllocTestScope {
+public:
+    AllocTestScope();
+    ~AllocTestScope();
+    AllocTestScope(const AllocTestScope &) = delete;
+    AllocTestScope &operator=(const AllocTestScope &) = delete;
+
+private:
+    bool outer_;
+};
+bool alloc_fails();     // counts one allocation; true when it is the one to fail
+void check_alloc();     // counts one allocation; throws std::bad_alloc when it is to fail
 
 // Validate `stream` and fill `v`; on failure sets the error message.
 ibp_status parse_stream(const void *stream, uint64_t stream_bytes, StreamView &v);

@@ -1,7 +1,8 @@
 // Compact device form of the clustered scheme's Mask/Bitval words, read by the row
 // gathers (the kernel side is load_row_meta / expand_row_meta in ibp_wave.hpp).
 //
-// A cluster stores one (Mask_w, Bitval_w) pair per 32-bit word w (Sec. 3.2). The words of
+// A cluster stores one (Mask_w, Bitval_w) pair per 32-bit word w (the Mask and Bitval of
+// Sec. 4.1, one pair per cluster as in the clustered compression of Sec. 6.5). The words of
 // a row repeat few distinct pairs (columns of one feature table share their invariant
 // exponent and mantissa bits), and a gather reads a cluster's metadata for every row it
 // decodes. So every cluster also gets a fixed-size slot, at g * slot bytes of the slot

@@ -31,6 +31,8 @@
 #include <mutex>
 #include <new>
 #include <thread>
+#include <unordered_map>
+#include <utility>
 #include <vector>
 
 #include <hip/hip_runtime.h>
@@ -72,6 +74,73 @@ hipError_t wait_event(hipEvent_t e) {
         if (r != hipErrorNotReady) return r;
         std::this_thread::yield();
     }
+}
+
+// Every device and pinned host allocation of the library goes through these, which keep
+// the byte counts that ibp_memory_usage reports and honour the allocation test hook.
+std::mutex g_mem_mu;
+std::unordered_map<void *, std::pair<uint64_t, bool>> g_mem;   // address -> (bytes, pinned)
+uint64_t g_dev_bytes = 0, g_pin_bytes = 0;
+
+bool track(void *p, uint64_t bytes, bool pinned) {
+    std::lock_guard<std::mutex> lock(g_mem_mu);
+    try {
+        g_mem.emplace(p, std::make_pair(bytes, pinned));
+    } catch (...) {
+        return false;
+    }
+    (pinned ? g_pin_bytes : g_dev_bytes) += bytes;
+    return true;
+}
+
+void untrack(void *p) {
+    std::lock_guard<std::mutex> lock(g_mem_mu);
+    auto it = g_mem.find(p);
+    if (it == g_mem.end()) return;
+    (it->second.second ? g_pin_bytes : g_dev_bytes) -= it->second.first;
+    g_mem.erase(it);
+}
+
+template <class T>
+hipError_t dev_alloc(T **p, uint64_t bytes) {
+    *p = nullptr;
+    if (alloc_fails()) return hipErrorOutOfMemory;
+    void *q = nullptr;
+    hipError_t e = hipMalloc(&q, bytes);
+    if (e != hipSuccess) return e;
+    if (!track(q, bytes, false)) {
+        ignore(hipFree(q));
+        return hipErrorOutOfMemory;
+    }
+    *p = static_cast<T *>(q);
+    return hipSuccess;
+}
+
+template <class T>
+hipError_t pinned_alloc(T **p, uint64_t bytes) {
+    *p = nullptr;
+    if (alloc_fails()) return hipErrorOutOfMemory;
+    void *q = nullptr;
+    hipError_t e = hipHostMalloc(&q, bytes, hipHostMallocDefault);
+    if (e != hipSuccess) return e;
+    if (!track(q, bytes, true)) {
+        ignore(hipHostFree(q));
+        return hipErrorOutOfMemory;
+    }
+    *p = static_cast<T *>(q);
+    return hipSuccess;
+}
+
+void dev_free(const void *p) {
+    if (!p) return;
+    untrack(const_cast<void *>(p));
+    ignore(hipFree(const_cast<void *>(p)));
+}
+
+void pinned_free(const void *p) {
+    if (!p) return;
+    untrack(const_cast<void *>(p));
+    ignore(hipHostFree(const_cast<void *>(p)));
 }
 
 }  // namespace
@@ -152,6 +221,9 @@ struct ibp_handle {
     std::vector<uint64_t> blk_off;         // packed bytes of every packing block (host gathers)
     std::vector<uint64_t> chunk_off;       // staged byte offset of every block of one chunk
     Pool *pool = nullptr;
+    // 0: free, 1: a call is running, 2: closed. A closed handle keeps this struct (its
+    // resources are freed), so later calls on it, a second ibp_close included, find the
+    // state and return IBP_ESTATE instead of touching freed memory.
     std::atomic<int> busy{0};
     int n_caches = 0;                      // live caches built on this handle
     ibp_stats stats{};
@@ -168,6 +240,7 @@ struct ibp_cache {
     unsigned long long *d_counts = nullptr;
     dev::CacheView view{};
     uint64_t rows = 0, slab_bytes = 0, slots = 0;
+    bool destroyed = false;   // kept as a marker after ibp_cache_destroy (under the handle's call)
 };
 
 namespace {
@@ -179,6 +252,7 @@ public:
         if (!h_) return;
         int expected = 0;
         ok_ = h_->busy.compare_exchange_strong(expected, 1);
+        closed_ = !ok_ && expected == 2;
         if (ok_) {
             ignore(hipGetDevice(&prev_));
             if (prev_ != h_->device) ignore(hipSetDevice(h_->device));
@@ -190,10 +264,12 @@ public:
         h_->busy.store(0);
     }
     bool ok() const { return ok_; }
+    bool closed() const { return closed_; }
 
 private:
     ibp_handle *h_;
     bool ok_ = false;
+    bool closed_ = false;
     int prev_ = -1;
 };
 
@@ -210,33 +286,62 @@ ibp_status hip_fail(ibp_handle *h, hipError_t e, const char *what) {
 
 ibp_status check_handle(ibp_handle *h, const CallScope &cs) {
     if (!h) return fail(IBP_EINVAL, "handle is null");
-    if (!cs.ok()) return fail(IBP_ESTATE, "handle is in use by another thread");
+    if (!cs.ok()) return fail(IBP_ESTATE, cs.closed() ? "handle is closed" : "handle is in use by another thread");
     if (h->sticky != hipSuccess)
         return fail(IBP_EHIP, std::string("earlier HIP error on this handle: ") + hipGetErrorString(h->sticky));
     return IBP_OK;
 }
 
-void free_handle(ibp_handle *h) {
-    if (!h) return;
-    ignore(hipFree(h->d_meta));
-    ignore(hipFree(h->d_slots));
-    ignore(hipFree(h->d_index));
-    ignore(hipFree(h->d_payload));
-    ignore(hipFree(h->d_err));
+// Frees everything a handle owns except the struct itself.
+void release_handle(ibp_handle *h) {
+    dev_free(h->d_meta);
+    dev_free(h->d_slots);
+    dev_free(h->d_index);
+    dev_free(h->d_payload);
+    dev_free(h->d_err);
+    h->d_meta = nullptr;
+    h->d_slots = nullptr;
+    h->d_index = nullptr;
+    h->d_payload = nullptr;
+    h->d_err = nullptr;
+    h->k_payload = nullptr;
     for (int j = 0; j < kIdSlots; ++j) {
-        ignore(hipFree(h->d_ids[j]));
-        if (h->h_ids[j]) ignore(hipHostFree(h->h_ids[j]));
+        dev_free(h->d_ids[j]);
+        pinned_free(h->h_ids[j]);
         if (h->ev_ids_free[j]) ignore(hipEventDestroy(h->ev_ids_free[j]));
+        h->d_ids[j] = nullptr;
+        h->h_ids[j] = nullptr;
+        h->ev_ids_free[j] = nullptr;
+        h->ids_cap[j] = 0;
     }
-    if (h->h_payload) ignore(hipHostFree(h->h_payload));
+    pinned_free(h->h_payload);
+    h->h_payload = nullptr;
     for (int b = 0; b < kStages; ++b) {
-        if (h->h_stage[b]) ignore(hipHostFree(h->h_stage[b]));
-        ignore(hipFree(h->d_stage[b]));
+        pinned_free(h->h_stage[b]);
+        dev_free(h->d_stage[b]);
         if (h->ev_copied[b]) ignore(hipEventDestroy(h->ev_copied[b]));
         if (h->ev_free[b]) ignore(hipEventDestroy(h->ev_free[b]));
+        h->h_stage[b] = nullptr;
+        h->d_stage[b] = nullptr;
+        h->ev_copied[b] = nullptr;
+        h->ev_free[b] = nullptr;
     }
     if (h->copy_stream) ignore(hipStreamDestroy(h->copy_stream));
+    h->copy_stream = nullptr;
     delete h->pool;
+    h->pool = nullptr;
+    std::vector<uint64_t>().swap(h->h_off);
+    std::vector<uint32_t>().swap(h->h_rb);
+    std::vector<uint32_t>().swap(h->req_g);
+    std::vector<uint32_t>().swap(h->req_rb);
+    std::vector<uint64_t>().swap(h->req_src);
+    std::vector<uint64_t>().swap(h->blk_off);
+    std::vector<uint64_t>().swap(h->chunk_off);
+}
+
+void free_handle(ibp_handle *h) {
+    if (!h) return;
+    release_handle(h);
     delete h;
 }
 
@@ -246,22 +351,25 @@ ibp_status claim_ids(ibp_handle *h, int j, uint64_t n) {
     if (h->ids_used[j]) IBP_HIP(h, wait_event(h->ev_ids_free[j]));
     if (n <= h->ids_cap[j]) return IBP_OK;
     uint64_t cap = std::max<uint64_t>(n, 2 * h->ids_cap[j]);
-    if (h->h_ids[j]) ignore(hipHostFree(h->h_ids[j]));
-    ignore(hipFree(h->d_ids[j]));
+    pinned_free(h->h_ids[j]);
+    dev_free(h->d_ids[j]);
     h->h_ids[j] = nullptr;
     h->d_ids[j] = nullptr;
     h->ids_cap[j] = 0;
-    if (hipHostMalloc((void **)&h->h_ids[j], cap * 8, hipHostMallocDefault) != hipSuccess)
+    if (pinned_alloc(&h->h_ids[j], cap * 8) != hipSuccess)
         return fail(IBP_ENOMEM, "pinned allocation for row ids failed");
-    if (hipMalloc((void **)&h->d_ids[j], cap * 8) != hipSuccess)
+    if (dev_alloc(&h->d_ids[j], cap * 8) != hipSuccess) {
+        pinned_free(h->h_ids[j]);      // a failed call holds nothing new
+        h->h_ids[j] = nullptr;
         return fail(IBP_ENOMEM, "device allocation for row ids failed");
+    }
     h->ids_cap[j] = cap;
     return IBP_OK;
 }
 
 ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
     const ibp_desc &d = h->d;
-    if (hipHostMalloc((void **)&h->h_payload, d.payload_bytes + kSlack, hipHostMallocDefault) != hipSuccess)
+    if (pinned_alloc(&h->h_payload, d.payload_bytes + kSlack) != hipSuccess)
         return fail(IBP_ENOMEM, "pinned allocation for the payload failed");
     const uint8_t *src = v.payload();
     uint8_t *dst = h->h_payload;
@@ -269,6 +377,7 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
         std::memcpy(dst + lo, src + lo, hi - lo);
     });
     std::memset(dst + d.payload_bytes, 0, kSlack);
+    check_alloc();
     if (d.flags & IBP_STREAM_PARTICIPATION) {
         h->h_off.resize(d.n_rows + 1);
         for (uint64_t r = 0; r <= d.n_rows; ++r) h->h_off[r] = v.off(r);
@@ -289,9 +398,9 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
     if ((uint64_t)d.row_bytes + 72 > kStageBytes)
         return fail(IBP_EINVAL, "rows larger than a staging buffer need another placement");
     for (int b = 0; b < kStages; ++b) {
-        if (hipHostMalloc((void **)&h->h_stage[b], kStageBytes + kSlack, hipHostMallocDefault) != hipSuccess)
+        if (pinned_alloc(&h->h_stage[b], kStageBytes + kSlack) != hipSuccess)
             return fail(IBP_ENOMEM, "pinned allocation for staging failed");
-        if (hipMalloc((void **)&h->d_stage[b], kStageBytes + kSlack) != hipSuccess)
+        if (dev_alloc(&h->d_stage[b], kStageBytes + kSlack) != hipSuccess)
             return fail(IBP_ENOMEM, "device allocation for staging failed");
         IBP_HIP(h, hipMemset(h->d_stage[b], 0, kStageBytes + kSlack));
         IBP_HIP(h, hipEventCreateWithFlags(&h->ev_copied[b], hipEventDisableTiming));
@@ -309,6 +418,7 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
 ibp_status setup_aligned_host_payload(ibp_handle *h, const StreamView &v) {
     const ibp_desc &d = h->d;
     const uint64_t ng = d.n_groups;
+    check_alloc();
     std::vector<uint64_t> aoff(ng + 1), rbs(ng);
     aoff[0] = 0;
     for (uint64_t g = 0; g < ng; ++g) {
@@ -316,7 +426,7 @@ ibp_status setup_aligned_host_payload(ibp_handle *h, const StreamView &v) {
         rbs[g] = (v.off(g + 1) - v.off(g)) / n;
         aoff[g + 1] = aoff[g] + n * ((rbs[g] + kRowAlign - 1) / kRowAlign * kRowAlign);
     }
-    if (hipHostMalloc((void **)&h->h_payload, aoff[ng] + kSlack, hipHostMallocDefault) != hipSuccess)
+    if (pinned_alloc(&h->h_payload, aoff[ng] + kSlack) != hipSuccess)
         return fail(IBP_ENOMEM, "pinned allocation for the aligned payload failed");
     const uint8_t *src = v.payload();
     uint8_t *dst = h->h_payload;
@@ -366,10 +476,13 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
     // one pass over the ids: cluster and packed size of every request, and the packed
     // bytes of every block
     const uint64_t nblk_all = (n + blk - 1) / blk;
+    // every host table of the call is sized here, before anything is enqueued
+    check_alloc();
     h->req_g.resize(n);
     h->req_rb.resize(n);
     h->req_src.resize(n);
     h->blk_off.assign(nblk_all + 1, 0);
+    h->chunk_off.resize((per_chunk + blk - 1) / blk + 1);
     uint32_t *rg = h->req_g.data(), *rrb = h->req_rb.data();
     uint64_t *rsrc = h->req_src.data();
     uint64_t *bs = h->blk_off.data();
@@ -427,8 +540,7 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
         // writes its tables and copies its rows (prefetching a few rows ahead, since each
         // row is a random read of ~rb bytes from host memory)
         const uint64_t k0 = i0 / blk, nblk = (nc + blk - 1) / blk;
-        h->chunk_off.resize(nblk + 1);
-        uint64_t *bo = h->chunk_off.data();
+        uint64_t *bo = h->chunk_off.data();   // sized for a whole chunk's blocks above
         bo[0] = 0;
         for (uint64_t k = 0; k < nblk; ++k) bo[k + 1] = bo[k] + bs[k0 + k + 1];
         const uint64_t total_pay = bo[nblk];
@@ -477,8 +589,15 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
 
 extern "C" {
 
-ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint32_t flags, ibp_handle **out) {
-    clear_error();
+}  // extern "C"
+
+namespace {
+
+// The body of ibp_open. `h` and `prev` are the caller's, so that it can also clean up after
+// an exception: h is the handle being built (null once freed here), prev the device that
+// was current before (-1 once restored here).
+ibp_status open_impl(const void *stream, uint64_t stream_bytes, int device, uint32_t flags, ibp_handle **out,
+                     ibp_handle *&h, int &prev) {
     if (!out) return fail(IBP_EINVAL, "handle output is null");
     *out = nullptr;
     if (flags != IBP_OPEN_PAYLOAD_DEVICE && flags != IBP_OPEN_PAYLOAD_HOST &&
@@ -496,33 +615,32 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     int count = 0;
     if (hipGetDeviceCount(&count) != hipSuccess || device < 0 || device >= count)
         return fail(IBP_EINVAL, "no such HIP device");
-    int prev = 0;
-    ignore(hipGetDevice(&prev));
+    int cur = 0;
+    ignore(hipGetDevice(&cur));
     if (hipSetDevice(device) != hipSuccess) return fail(IBP_EHIP, "hipSetDevice failed");
+    prev = cur;
     int64_t *scratch_ids = nullptr;
     const hipError_t scratch_err = scratch_on_device(device, &scratch_ids);
 
-    ibp_handle *h = new (std::nothrow) ibp_handle();
-    if (!h) {
+    auto bail = [&](ibp_status s) {
+        free_handle(h);
+        h = nullptr;
         ignore(hipSetDevice(prev));
-        return fail(IBP_ENOMEM, "host allocation failed");
-    }
+        prev = -1;
+        return s;
+    };
+    if (alloc_fails() || !(h = new (std::nothrow) ibp_handle())) return bail(fail(IBP_ENOMEM, "host allocation failed"));
     h->device = device;
     h->flags = flags;
     h->scratch_ids = scratch_ids;
     h->scratch_err = scratch_err;
     h->d = d;
+    check_alloc();
     h->pool = new Pool(std::min(16, online_cpus()));
-    auto bail = [&](ibp_status s) {
-        free_handle(h);
-        ignore(hipSetDevice(prev));
-        return s;
-    };
     const uint64_t meta_bytes = d.n_groups * 2ull * d.row_bytes;
     const uint64_t n_index = (d.flags & IBP_STREAM_PARTICIPATION) ? d.n_rows + 1 : d.n_groups + 1;
-    if (hipMalloc((void **)&h->d_meta, std::max<uint64_t>(meta_bytes, 4)) != hipSuccess ||
-        hipMalloc((void **)&h->d_index, 8 * n_index) != hipSuccess ||
-        hipMalloc((void **)&h->d_err, 8) != hipSuccess)
+    if (dev_alloc(&h->d_meta, std::max<uint64_t>(meta_bytes, 4)) != hipSuccess ||
+        dev_alloc(&h->d_index, 8 * n_index) != hipSuccess || dev_alloc(&h->d_err, 8) != hipSuccess)
         return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
     if (meta_bytes && hipMemcpy(h->d_meta, v.meta(), meta_bytes, hipMemcpyHostToDevice) != hipSuccess)
         return bail(fail(IBP_EHIP, "metadata upload failed"));
@@ -534,10 +652,11 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
         // the row gathers read a cluster's metadata for every row they decode: when every
         // cluster fits one, give each a compact slot as well
         const uint32_t K = (uint32_t)dev::words_per_lane(W);
+        check_alloc();
         std::vector<uint8_t> slots;
         const uint32_t P = build_meta_slots(v.meta(), d.n_groups, W, K, *h->pool, slots);
         if (P) {
-            if (hipMalloc((void **)&h->d_slots, slots.size()) != hipSuccess)
+            if (dev_alloc(&h->d_slots, slots.size()) != hipSuccess)
                 return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
             if (hipMemcpy(h->d_slots, slots.data(), slots.size(), hipMemcpyHostToDevice) != hipSuccess)
                 return bail(fail(IBP_EHIP, "metadata upload failed"));
@@ -547,7 +666,7 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     }
     if (flags == IBP_OPEN_PAYLOAD_DEVICE) {
         const uint64_t bytes = round_up(d.payload_bytes + kSlack, 256);
-        if (hipMalloc((void **)&h->d_payload, bytes) != hipSuccess)
+        if (dev_alloc(&h->d_payload, bytes) != hipSuccess)
             return bail(fail(IBP_ENOMEM, "device allocation for the payload failed"));
         if (hipMemset(h->d_payload + d.payload_bytes, 0, bytes - d.payload_bytes) != hipSuccess ||
             (d.payload_bytes &&
@@ -580,8 +699,27 @@ ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint3
     h->ds.W = d.row_bytes / 4;
     h->ds.G = d.group_rows;
     ignore(hipSetDevice(prev));
+    prev = -1;
     *out = h;
     return IBP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ibp_status ibp_open(const void *stream, uint64_t stream_bytes, int device, uint32_t flags, ibp_handle **out) {
+    clear_error();
+    AllocTestScope scope;
+    ibp_handle *h = nullptr;
+    int prev = -1;
+    const ibp_status st = guarded([&] { return open_impl(stream, stream_bytes, device, flags, out, h, prev); });
+    if (st != IBP_OK) {
+        if (h) free_handle(h);
+        if (prev >= 0) ignore(hipSetDevice(prev));
+        if (out) *out = nullptr;
+    }
+    return st;
 }
 
 ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, void *d_out, uint64_t out_cap,
@@ -647,9 +785,12 @@ ibp_status ibp_decompress(ibp_handle *h, uint64_t first_row, uint64_t n_rows, vo
     return IBP_OK;
 }
 
-ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, void *d_out,
-                                 uint64_t out_cap, void *stream) {
-    clear_error();
+}  // extern "C"
+
+namespace {
+
+ibp_status gather_impl(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, void *d_out, uint64_t out_cap,
+                       void *stream) {
     CallScope cs(h);
     ibp_status st = check_handle(h, cs);
     if (st != IBP_OK) return st;
@@ -682,6 +823,17 @@ ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t
     h->stats.rows_out += n_ids;
     h->stats.out_bytes += n_ids * L;
     return IBP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ibp_status ibp_gather_decompress(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, void *d_out,
+                                 uint64_t out_cap, void *stream) {
+    clear_error();
+    AllocTestScope scope;
+    return guarded([&] { return gather_impl(h, row_ids, n_ids, d_out, out_cap, stream); });
 }
 
 ibp_status ibp_gather_decompress_device(ibp_handle *h, const int64_t *d_row_ids, uint64_t n_ids, void *d_out,
@@ -751,14 +903,20 @@ ibp_status ibp_device_errors(ibp_handle *h, uint64_t *count) {
 
 ibp_status ibp_get_desc(ibp_handle *h, ibp_desc *d) {
     clear_error();
-    if (!h || !d) return fail(IBP_EINVAL, "null argument");
+    if (!d) return fail(IBP_EINVAL, "null argument");
+    CallScope cs(h);
+    if (!h) return fail(IBP_EINVAL, "handle is null");
+    if (!cs.ok()) return fail(IBP_ESTATE, cs.closed() ? "handle is closed" : "handle is in use by another thread");
     *d = h->d;
     return IBP_OK;
 }
 
 ibp_status ibp_get_stats(ibp_handle *h, ibp_stats *st) {
     clear_error();
-    if (!h || !st) return fail(IBP_EINVAL, "null argument");
+    if (!st) return fail(IBP_EINVAL, "null argument");
+    CallScope cs(h);
+    if (!h) return fail(IBP_EINVAL, "handle is null");
+    if (!cs.ok()) return fail(IBP_ESTATE, cs.closed() ? "handle is closed" : "handle is in use by another thread");
     *st = h->stats;
     st->gather_meta_bytes = h->d_slots ? h->ds.slot_bytes : 2ull * h->d.row_bytes;
     return IBP_OK;
@@ -766,7 +924,9 @@ ibp_status ibp_get_stats(ibp_handle *h, ibp_stats *st) {
 
 ibp_status ibp_reset_stats(ibp_handle *h) {
     clear_error();
-    if (!h) return fail(IBP_EINVAL, "null argument");
+    CallScope cs(h);
+    if (!h) return fail(IBP_EINVAL, "handle is null");
+    if (!cs.ok()) return fail(IBP_ESTATE, cs.closed() ? "handle is closed" : "handle is in use by another thread");
     h->stats = ibp_stats{};
     return IBP_OK;
 }
@@ -776,7 +936,7 @@ ibp_status ibp_close(ibp_handle *h) {
     if (!h) return IBP_OK;
     int expected = 0;
     if (!h->busy.compare_exchange_strong(expected, 1))
-        return fail(IBP_ESTATE, "handle is in use by another thread");
+        return fail(IBP_ESTATE, expected == 2 ? "handle is already closed" : "handle is in use by another thread");
     if (h->n_caches) {
         h->busy.store(0);
         return fail(IBP_ESTATE, "destroy the caches built on this handle first");
@@ -785,16 +945,29 @@ ibp_status ibp_close(ibp_handle *h) {
     ignore(hipGetDevice(&prev));
     ignore(hipSetDevice(h->device));
     hipError_t e = hipDeviceSynchronize();
-    free_handle(h);
+    release_handle(h);
     ignore(hipSetDevice(prev));
+    h->busy.store(2);   // the struct stays as the closed marker
     if (e != hipSuccess) return fail(IBP_EHIP, std::string("pending work failed: ") + hipGetErrorString(e));
+    return IBP_OK;
+}
+
+ibp_status ibp_memory_usage(uint64_t *device_bytes, uint64_t *pinned_bytes) {
+    clear_error();
+    if (!device_bytes || !pinned_bytes) return fail(IBP_EINVAL, "null argument");
+    std::lock_guard<std::mutex> lock(g_mem_mu);
+    *device_bytes = g_dev_bytes;
+    *pinned_bytes = g_pin_bytes;
     return IBP_OK;
 }
 
 // ---- compressed device cache ---------------------------------------------------
 
-ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, ibp_cache **out) {
-    clear_error();
+}  // extern "C"
+
+namespace {
+
+ibp_status cache_create_impl(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, ibp_cache **out) {
     if (!out) return fail(IBP_EINVAL, "cache output is null");
     *out = nullptr;
     CallScope cs(h);
@@ -811,6 +984,7 @@ ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_id
         if (row_ids[i] < 0 || (uint64_t)row_ids[i] >= d.n_rows)
             return fail(IBP_ERANGE, "row id " + std::to_string(row_ids[i]) + " at position " + std::to_string(i) +
                                         " is outside [0, " + std::to_string(d.n_rows) + ")");
+    check_alloc();
     std::vector<int64_t> ids(row_ids, row_ids + n_ids);
     std::sort(ids.begin(), ids.end());
     ids.erase(std::unique(ids.begin(), ids.end()), ids.end());
@@ -833,6 +1007,7 @@ ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_id
     std::vector<uint8_t> slab;
     std::vector<Slot> table;
     try {
+        check_alloc();
         slab.assign(dst[n] + kSlack, 0);
         table.assign(cap, Slot{0, 0});
     } catch (const std::bad_alloc &) {
@@ -848,18 +1023,17 @@ ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_id
         // entry: slab byte offset (bits 0-39), slab 0 (bits 40-42), compressed form (bit 43)
         table[k] = Slot{id + 1, dst[i] | (1ull << 43)};
     }
-    auto *c = new (std::nothrow) ibp_cache();
+    auto *c = alloc_fails() ? nullptr : new (std::nothrow) ibp_cache();
     if (!c) return fail(IBP_ENOMEM, "host allocation failed");
     auto bail = [&](ibp_status e) {
-        ignore(hipFree(c->d_slab));
-        ignore(hipFree(c->d_table));
-        ignore(hipFree(c->d_counts));
+        dev_free(c->d_slab);
+        dev_free(c->d_table);
+        dev_free(c->d_counts);
         delete c;
         return e;
     };
-    if (hipMalloc((void **)&c->d_slab, slab.size()) != hipSuccess ||
-        hipMalloc(&c->d_table, cap * sizeof(Slot)) != hipSuccess ||
-        hipMalloc((void **)&c->d_counts, kCountBytes) != hipSuccess)
+    if (dev_alloc(&c->d_slab, slab.size()) != hipSuccess || dev_alloc(&c->d_table, cap * sizeof(Slot)) != hipSuccess ||
+        dev_alloc(&c->d_counts, kCountBytes) != hipSuccess)
         return bail(fail(IBP_ENOMEM, "device allocation for the cache failed"));
     if (hipMemcpy(c->d_slab, slab.data(), slab.size(), hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(c->d_table, table.data(), cap * sizeof(Slot), hipMemcpyHostToDevice) != hipSuccess ||
@@ -880,6 +1054,16 @@ ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_id
     return IBP_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+ibp_status ibp_cache_create(ibp_handle *h, const int64_t *row_ids, uint64_t n_ids, ibp_cache **out) {
+    clear_error();
+    AllocTestScope scope;
+    return guarded([&] { return cache_create_impl(h, row_ids, n_ids, out); });
+}
+
 ibp_status ibp_cache_gather(ibp_cache *c, const int64_t *d_row_ids, uint64_t n_ids, void *d_out, uint64_t out_cap,
                             void *stream) {
     clear_error();
@@ -888,6 +1072,7 @@ ibp_status ibp_cache_gather(ibp_cache *c, const int64_t *d_row_ids, uint64_t n_i
     CallScope cs(h);
     ibp_status st = check_handle(h, cs);
     if (st != IBP_OK) return st;
+    if (c->destroyed) return fail(IBP_ESTATE, "cache is destroyed");
     if (n_ids == 0) return IBP_OK;
     if (!d_row_ids || !d_out) return fail(IBP_EINVAL, "row ids or output is null");
     if (out_cap / h->d.row_bytes < n_ids) return fail(IBP_ENOMEM, "output capacity too small");
@@ -905,6 +1090,7 @@ ibp_status ibp_cache_get_stats(ibp_cache *c, ibp_cache_stats *st) {
     CallScope cs(c->h);
     ibp_status s = check_handle(c->h, cs);
     if (s != IBP_OK) return s;
+    if (c->destroyed) return fail(IBP_ESTATE, "cache is destroyed");
     unsigned long long counts[dev::kCountLines * dev::kCountStride];
     IBP_HIP(c->h, hipDeviceSynchronize());
     IBP_HIP(c->h, hipMemcpy(counts, c->d_counts, kCountBytes, hipMemcpyDeviceToHost));
@@ -925,6 +1111,7 @@ ibp_status ibp_cache_reset_stats(ibp_cache *c) {
     CallScope cs(c->h);
     ibp_status s = check_handle(c->h, cs);
     if (s != IBP_OK) return s;
+    if (c->destroyed) return fail(IBP_ESTATE, "cache is destroyed");
     IBP_HIP(c->h, hipDeviceSynchronize());
     IBP_HIP(c->h, hipMemset(c->d_counts, 0, kCountBytes));
     return IBP_OK;
@@ -935,13 +1122,18 @@ ibp_status ibp_cache_destroy(ibp_cache *c) {
     if (!c) return IBP_OK;
     ibp_handle *h = c->h;
     CallScope cs(h);
-    if (!cs.ok()) return fail(IBP_ESTATE, "the cache's handle is in use by another thread");
+    if (!cs.ok())
+        return fail(IBP_ESTATE, cs.closed() ? "the cache's handle is closed" : "the cache's handle is in use by another thread");
+    if (c->destroyed) return fail(IBP_ESTATE, "cache is already destroyed");
     hipError_t e = hipDeviceSynchronize();
-    ignore(hipFree(c->d_slab));
-    ignore(hipFree(c->d_table));
-    ignore(hipFree(c->d_counts));
+    dev_free(c->d_slab);
+    dev_free(c->d_table);
+    dev_free(c->d_counts);
+    c->d_slab = nullptr;
+    c->d_table = nullptr;
+    c->d_counts = nullptr;
     --h->n_caches;
-    delete c;
+    c->destroyed = true;   // the struct stays as the destroyed marker
     if (e != hipSuccess) return fail(IBP_EHIP, std::string("pending work failed: ") + hipGetErrorString(e));
     return IBP_OK;
 }

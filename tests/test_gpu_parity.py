@@ -281,26 +281,63 @@ def _full_stream(cfg):
     return rows, stream, d
 
 
-@pytest.mark.timeout(900)
+MODE_FLAGS = {"device_ids": ibp.IBP_OPEN_PAYLOAD_DEVICE, "host_ids": ibp.IBP_OPEN_PAYLOAD_DEVICE,
+              "host_payload": ibp.IBP_OPEN_PAYLOAD_HOST,
+              "zero_copy_device_ids": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY,
+              "zero_copy_host_ids": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY,
+              "zero_copy_aligned_device_ids": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED}
+
+
+def _full_gathers(torch, key, stream, ids, want, L, modes):
+    """One batch through every mode; each output must equal the original rows."""
+    for mode in modes:
+        say(f"[{key}] gather mode={mode} n_ids={ids.size}")
+        got, errs = gpu_gather(torch, stream, ids, L, MODE_FLAGS[mode], device_ids=mode.endswith("device_ids"))
+        assert errs == 0
+        assert np.array_equal(got, want), mode
+        del got
+
+
+def _full_participation(torch, key, rows, ids, want, L):
+    """The thresholded scheme at full size (one global Mask sampled from every row,
+    T = 4/5, 8-byte chunks): the same batch through every placement it supports, and a
+    sample of rows decoded by the oracle from the library's stream."""
+    import gc
+    import time
+    t = time.time()
+    ps = ibp.ibp_compress_ex(rows, rows.shape[0], chunk_bytes=8, threshold=(4, 5))
+    d = ibp.ibp_describe(ps)
+    say(f"[{key}] thresholded stream in {time.time() - t:.0f}s: payload {d['payload_bytes'] / 1e9:.2f} GB")
+    sample = np.random.default_rng(13).choice(ids.size, 2000, replace=False)
+    assert np.array_equal(oracle.decode_rows(ps, ids[sample], L), want[sample])
+    _full_gathers(torch, key + " thresholded", ps, ids, want, L,
+                  ("device_ids", "host_ids", "host_payload", "zero_copy_device_ids"))
+    del ps
+    gc.collect()
+
+
+@pytest.mark.timeout(1200)
 def test_dlrm_full(torch):
     """26 tables x 4M rows x 128 fp32 (53 GB raw), one batch of 2,048 x 26 Zipf lookups."""
     import gc
+    import stream_check
     from workloads import dlrm_batch_ids
     cfg = CONFIGS["dlrm"]
+    G, L = cfg.group_rows, cfg.row_bytes
     rows, stream, d = _full_stream(cfg)
-    _sampled_groups_match_oracle(stream, rows, cfg.group_rows, cfg.row_bytes, d["n_groups"], 48, 7)
     x = cfg.extra
     ids = dlrm_batch_ids(x["tables"], x["rows_per_table"], x["batch"], x["zipf_s"], batch_index=0)
+    # stream identity: runs covering 1% of the clusters, plus every cluster the batch touches
+    runs = stream_check.sampled_runs(d["n_groups"], 0.01, 50, seed=7, must=ids // G)
+    heads = stream_check.check_runs(stream, rows, G, runs)
+    say(f"[dlrm] {sum(b - a for a, b in runs)} of {d['n_groups']} clusters identical to the oracle's "
+        f"({len(heads)} runs)")
     want = rows[ids]
     sample = np.random.default_rng(9).choice(ids.size, 2000, replace=False)
-    assert np.array_equal(oracle.decode_rows(stream, ids[sample], cfg.row_bytes), want[sample])
-    for mode in ("device_ids", "zero_copy_device_ids", "zero_copy_aligned_device_ids"):
-        say(f"[dlrm] gather mode={mode} n_ids={ids.size}")
-        flags = (ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED if mode.startswith("zero_copy_aligned") else
-                 ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
-        got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=True)
-        assert errs == 0
-        assert np.array_equal(got, want)       # [2048, 26, 128] fp32, sample-major
+    assert np.array_equal(oracle.decode_rows(stream, ids[sample], L), want[sample])
+    _full_gathers(torch, "dlrm", stream, ids, want, L,
+                  ("device_ids", "host_ids", "host_payload", "zero_copy_device_ids", "zero_copy_host_ids",
+                   "zero_copy_aligned_device_ids"))
     # the compressed device cache over the full tables: the 2M most popular rows cached,
     # hits decoded from HBM and misses from pinned host memory in one kernel
     from workloads import dlrm_hot_order
@@ -309,37 +346,45 @@ def test_dlrm_full(torch):
     with ibp.ibp_open(stream, 0, ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) as h:
         with ibp.ibp_cache_create(h, hot) as c:
             d_ids = torch.from_numpy(ids).cuda()
-            out = torch.empty(ids.size * cfg.row_bytes, dtype=torch.uint8, device="cuda")
+            out = torch.empty(ids.size * L, dtype=torch.uint8, device="cuda")
             ibp.ibp_cache_gather(c, d_ids, out)
             torch.cuda.synchronize()
-            assert np.array_equal(out.cpu().numpy().reshape(-1, cfg.row_bytes), want)
+            assert np.array_equal(out.cpu().numpy().reshape(-1, L), want)
             st = ibp.ibp_cache_get_stats(c)
             hits = int(np.isin(ids, hot).sum())
             assert st["hits"] == hits and st["misses"] == ids.size - hits and hits > ids.size // 2
         assert ibp.ibp_device_errors(h) == 0
-    del rows, stream
+    del stream
+    gc.collect()
+    _full_participation(torch, "dlrm", rows, ids, want, L)
+    del rows
     gc.collect()
 
 
-@pytest.mark.timeout(900)
+@pytest.mark.timeout(1200)
 def test_big_gnn_full(torch):
-    """111M rows x 128 fp32 (57 GB raw), G = 64, a 3-hop (15,10,5) minibatch of ~3.69M rows."""
+    """111M rows x 128 fp32 (57 GB raw), G = 64, a 3-hop (15,10,5) minibatch of ~3.69M
+    rows: every placement, including the staged one, whose ~0.94 GB of packed rows cross
+    PCIe in about eight 128 MiB stages."""
     import gc
+    import stream_check
     cfg = CONFIGS["big_gnn"]
+    G, L = cfg.group_rows, cfg.row_bytes
     rows, stream, d = _full_stream(cfg)
-    _sampled_groups_match_oracle(stream, rows, cfg.group_rows, cfg.row_bytes, d["n_groups"], 48, 8)
+    runs = stream_check.sampled_runs(d["n_groups"], 0.01, 50, seed=8)
+    stream_check.check_runs(stream, rows, G, runs)
+    say(f"[big_gnn] {sum(b - a for a, b in runs)} of {d['n_groups']} clusters identical to the oracle's")
     ids = gnn_batch_ids(cfg.n_rows, cfg.extra["seeds"], cfg.extra["fanouts"], batch_index=0)
     want = rows[ids]
     sample = np.random.default_rng(10).choice(ids.size, 2000, replace=False)
-    assert np.array_equal(oracle.decode_rows(stream, ids[sample], cfg.row_bytes), want[sample])
-    for mode in ("device_ids", "zero_copy_device_ids", "zero_copy_aligned_device_ids"):
-        say(f"[big_gnn] gather mode={mode} n_ids={ids.size}")
-        flags = (ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED if mode.startswith("zero_copy_aligned") else
-                 ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY if mode.startswith("zero") else ibp.IBP_OPEN_PAYLOAD_DEVICE)
-        got, errs = gpu_gather(torch, stream, ids, cfg.row_bytes, flags, device_ids=True)
-        assert errs == 0
-        assert np.array_equal(got, want)
-    del rows, stream, want
+    assert np.array_equal(oracle.decode_rows(stream, ids[sample], L), want[sample])
+    _full_gathers(torch, "big_gnn", stream, ids, want, L,
+                  ("device_ids", "host_ids", "host_payload", "zero_copy_device_ids", "zero_copy_host_ids",
+                   "zero_copy_aligned_device_ids"))
+    del stream
+    gc.collect()
+    _full_participation(torch, "big_gnn", rows, ids, want, L)
+    del rows, want
     gc.collect()
 
 

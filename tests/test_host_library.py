@@ -192,3 +192,81 @@ def test_kernel_code_hash_ignores_comments_only():
     assert bench.code_sha256([src]) == bench.code_sha256([same])
     assert bench.code_sha256([src]) != bench.code_sha256([other])
     assert len(bench.kernel_sources_sha256()) == 64
+
+
+def test_binding_rejects_host_buffers_for_device_arguments():
+    """Device arguments are checked in the binding before any address reaches the library:
+    CPU tensors, numpy arrays, int32 ids and strided views are refused with TypeError."""
+    import torch
+    h = ibp.Handle(None)
+    ids64 = torch.arange(4, dtype=torch.int64)
+    out = torch.empty(4 * 64, dtype=torch.uint8)
+    for call in (lambda: ibp.ibp_gather_decompress_device(h, ids64, out),
+                 lambda: ibp.ibp_decompress(h, 0, 4, out),
+                 lambda: ibp.ibp_decompress(h, 0, 4, np.zeros(256, np.uint8)),
+                 lambda: ibp.ibp_gather_decompress(h, np.arange(4), out),
+                 lambda: ibp.ibp_gather_decompress_noalloc(h, np.arange(4), out),
+                 lambda: ibp.ibp_cache_gather(ibp.Cache(None, h), ids64, out),
+                 lambda: ibp.ibp_gather_decompress_device(h, ids64.to(torch.int32), out),
+                 lambda: ibp.ibp_gather_decompress_device(h, torch.arange(8, dtype=torch.int64)[::2], out)):
+        with pytest.raises(TypeError):
+            call()
+
+
+@pytest.mark.parametrize("scheme", ["clustered", "participation"])
+def test_compress_allocation_failure_writes_nothing(scheme, monkeypatch):
+    """IBP_TEST_FAIL_ALLOC=n fails the n-th allocation of one compress call: IBP_ENOMEM and
+    an untouched output, for every n up to the call's allocation count; beyond it the
+    stream equals the oracle's."""
+    import ctypes
+    rows = structured_rows("floats", 300, 64, seed=9)
+    if scheme == "participation":
+        want = oracle.compress(rows, 300, chunk_bytes=8, threshold=(4, 5))
+        p = ibp.ibp_params(300, 8, 4, 5, 1)
+        call = lambda buf, got: ibp.lib().ibp_compress_ex(rows.ctypes.data, 300, 64, ctypes.byref(p), 1,
+                                                          buf.ctypes.data, buf.size, ctypes.byref(got))
+    else:
+        want = oracle.compress(rows, 16)
+        call = lambda buf, got: ibp.lib().ibp_compress(rows.ctypes.data, 300, 64, 16, 1, buf.ctypes.data,
+                                                       buf.size, ctypes.byref(got))
+    failures = 0
+    for n in range(1, 10):
+        monkeypatch.setenv("IBP_TEST_FAIL_ALLOC", str(n))
+        buf = np.full(want.size, 0xAB, np.uint8)
+        got = ctypes.c_uint64(0)
+        st = call(buf, got)
+        if st == ibp.IBP_OK:
+            assert np.array_equal(buf, want)
+            break
+        assert st == ibp.IBP_ENOMEM, st
+        assert (buf == 0xAB).all(), n
+        failures += 1
+    else:
+        raise AssertionError("the call never succeeded")
+    assert failures >= 2
+    monkeypatch.delenv("IBP_TEST_FAIL_ALLOC")
+    assert np.array_equal(ibp.ibp_compress_ex(rows, 300, 8, (4, 5)) if scheme == "participation"
+                          else ibp.ibp_compress(rows, 16), want)
+
+
+def test_memory_usage_without_handles():
+    dev, pin = ibp.ibp_memory_usage()
+    assert dev == 0 and pin == 0
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("key", ["gnn_gather", "kv_bf16"])
+def test_whole_workload_stream_matches_oracle(key):
+    """The whole 2.4M x 400 B GNN table and the whole 4 GiB bf16 KV cache: the library's
+    stream equals the oracle's byte for byte (every cluster's metadata, index and packed
+    rows, and the header), the oracle running on cluster runs in parallel threads."""
+    import time
+    import stream_check
+    from workloads import gen_all_rows
+    cfg = CONFIGS[key]
+    rows = gen_all_rows(cfg)
+    stream = ibp.ibp_compress(rows, cfg.group_rows)
+    t = time.time()
+    ng = stream_check.check_whole(stream, rows, cfg.group_rows, pieces=256, threads=min(16, os.cpu_count() or 1))
+    assert ng == (cfg.n_rows + cfg.group_rows - 1) // cfg.group_rows
+    print(f"{key}: {ng} clusters identical to the oracle's in {time.time() - t:.1f}s")
