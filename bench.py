@@ -1,17 +1,21 @@
 #!/usr/bin/env python3
 """Benchmark of the IBP decompression hot path on one MI355X.
 
-Default workload (`--workload gnn_gather`): the GNN minibatch gather -- 2,400,000 rows x
-100 fp32 features (N(0,1) rounded to 8 mantissa bits), clusters of 32 rows, minibatches of
-1,024 seed rows with a 2-hop (15, 10) uniform fanout (about 164k unique sorted row ids).
-The compressed stream and every batch's ids are resident in HBM before timing starts; one
-step = one ibp_gather_decompress_device call over one minibatch (a different batch each
-step). `value` is decompressed output bytes per second over the timed steps.
+Headline workload (the default run): the large GNN feature gather -- 111,000,000 rows x
+128 fp32 features (70% zeros, the rest U(0,1) in 1/1024 steps), clusters of 64 rows,
+minibatches of 4,096 seed rows with a 3-hop (15, 10, 5) uniform fanout (about 3.69M unique
+sorted row ids). The compressed stream and every batch's ids are resident in HBM before
+timing starts; one step = one ibp_gather_decompress_device call over one minibatch (a
+different batch each step). `value` is decompressed output bytes per second over the
+timed steps.
 
-Other workloads (`--workload`): `dlrm` (26 tables x 4M x 128 fp32, batches of 2,048 x 26
-Zipf lookups), `big_gnn` (111M x 128 fp32, 3-hop minibatches), both gathers like the
-default; `kv_bf16` (one step = one 128 MiB layer of the bf16 KV cache through
-ibp_decompress) and `tiny_gnn` (one step = the whole 4,096 x 128 fp32 tensor).
+The default run then measures the other four workloads the same way (without the CPU
+oracle leg, with at least 200 timed steps each) and reports them under `other_configs`,
+within --budget-s of wall time:
+`tiny_gnn` (one step = the whole 4,096 x 128 fp32 tensor), `gnn_gather` (2.4M x 100 fp32,
+2-hop minibatches of ~164k rows), `kv_bf16` (one step = one 128 MiB layer of the bf16 KV
+cache through ibp_decompress) and `dlrm` (26 tables x 4M x 128 fp32, batches of 2,048 x 26
+Zipf lookups). `--workload W` measures only W, as the headline.
 
 Also reported on the same JSON line:
   roofline      the step kernel's algorithmic HBM bytes per launch over its average
@@ -78,6 +82,11 @@ def code_sha256(texts):
 def kernel_sources_sha256():
     return code_sha256(open(path).read() for path in KERNEL_SOURCES)
 GATHERS = ("gnn_gather", "dlrm", "big_gnn")
+HEADLINE = "big_gnn"        # the largest configuration that fits one GPU
+OTHERS = ("tiny_gnn", "gnn_gather", "kv_bf16", "dlrm")
+# seconds a workload usually takes end to end in the default run (drawing, compressing,
+# every leg), so the run stops starting new ones before the budget runs out
+BUDGET_NEEDS = {"tiny_gnn": 15, "gnn_gather": 40, "kv_bf16": 60, "dlrm": 150}
 STREAMS = ("kv_bf16", "tiny_gnn")
 DESCRIPTIONS = {
     "gnn_gather": "gnn_gather: 2.4M x 100 fp32 rows (N(0,1), 8 mantissa bits), G=32, 1,024 seeds, "
@@ -609,7 +618,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="gnn_gather", choices=list(GATHERS + STREAMS))
+    ap.add_argument("--workload", default=None, choices=list(GATHERS + STREAMS),
+                    help="measure only this workload (default: the 111M-row GNN gather as the headline, "
+                         "then the other four under other_configs)")
+    ap.add_argument("--budget-s", type=float, default=480.0,
+                    help="wall-clock budget of the default run: a further workload starts only while "
+                         "its usual time is left")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target length of the CPU oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-e2e", action="store_true")
@@ -646,14 +660,40 @@ def main():
         cache_bench(args)
         return
 
+    if args.workload:
+        line = run_workload(args, args.workload, args.steps, args.warmup)
+    else:
+        t_start = time.time()
+        line = run_workload(args, HEADLINE, args.steps, args.warmup)
+        others = {}
+        for wl in OTHERS:
+            left = args.budget_s - (time.time() - t_start)
+            if left < BUDGET_NEEDS[wl]:
+                others[wl] = {"skipped": f"time budget ({left:.0f} s left of --budget-s {args.budget_s:.0f})"}
+                log(f"[bench] {wl}: skipped, {left:.0f} s left")
+                continue
+            # at least 200 timed steps: the short lookups of the DLRM batches need that many
+            # to reach their steady state (20 steps read ~60% slower), and they cost ~5 ms
+            k_w, w_w = max(args.steps, 200), max(args.warmup, 20)
+            r = run_workload(args, wl, k_w, w_w, with_cpu=False)
+            others[wl] = {"steps": k_w, "warmup": w_w,
+                          **{k: r[k] for k in ("value", "unit", "ms_per_step", "config", "roofline",
+                                               "uncompressed_device", "plain_gather", "e2e")}}
+        line["other_configs"] = others
+        line["bench_wall_s"] = round(time.time() - t_start, 1)
+    print(json.dumps(line), flush=True)
+
+
+def run_workload(args, wl, K, Wm, with_cpu=True):
+    """One workload's bench line (a dict): the device-resident steps, the uncompressed
+    and plain-gather baselines, the CPU oracle (when with_cpu) and the PCIe legs."""
+    import gc
     import torch
     import paper_2605_30728_amd as ibp
     from workloads import CONFIGS, gen_all_rows
 
-    wl = args.workload
     cfg = CONFIGS[wl]
     G, L, W = cfg.group_rows, cfg.row_bytes, cfg.row_bytes // 4
-    K, Wm = args.steps, args.warmup
     t = time.time()
     rows = gen_all_rows(cfg)
     log(f"[bench] {wl}: generated {cfg.n_rows} x {L} B rows in {time.time() - t:.1f}s")
@@ -750,7 +790,7 @@ def main():
         f"plain 1 GiB d2d copy {copy_gbs:.0f} GB/s")
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if with_cpu and not args.no_cpu_baseline:
         kw = ({"chunk_bytes": args.chunk_bytes, "threshold": (num, den), "sample_every": args.sample_every}
               if part else None)
         cpu = cpu_baseline(stream, rows, steps, last, L, G, args.cpu_seconds, kw)
@@ -785,7 +825,14 @@ def main():
         "cpu_baseline": cpu,
         "e2e": e2e,
     }
-    print(json.dumps(line), flush=True)
+    del rows, stream, ident, out
+    if wl in GATHERS:
+        del d_units
+    gc.collect()
+    torch.cuda.empty_cache()
+    return line
+
+
 
 
 if __name__ == "__main__":
