@@ -387,7 +387,9 @@ def pcie_legs(torch, ibp, args, stream, ident, rows, steps, L, layout):
 
     def leg(src, flags, check):
         h = ibp.ibp_open(src, 0, flags)
-        for k in sel[:3]:
+        # ten untimed steps: the first tens of milliseconds after opening a handle run
+        # slower (host threads and the copy path warming up), three steps measured too few
+        for k in sel[:10]:
             run(h, k)
         torch.cuda.synchronize()
         ibp.ibp_reset_stats(h)
