@@ -144,9 +144,7 @@ __device__ __forceinline__ void decode_batch(const Tile<K, MAXR> &t, const uint3
 #pragma unroll
         for (int j = 0; j < K; ++j) {
             b[i][j] = bit0 + t.s[j];
-            const uint32_t q = b[i][j] >> 5;
-            d0[i][j] = p[q];
-            d1[i][j] = p[q + 1];
+            load_window(p, b[i][j] >> 5, d0[i][j], d1[i][j]);
         }
     }
 #pragma unroll
@@ -488,13 +486,11 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
                                      (uint32_t)__builtin_amdgcn_readlane((int)off_lo, (int)i);
                 rbyte = off + (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)r_l, (int)i) * rb;
             }
-            const uint32_t *__restrict__ p = pay32 + (rbyte >> 2);
             bit0[u] = ((uint32_t)rbyte & 3u) * 8u;
+            const __amdgpu_buffer_rsrc_t rr = row_rsrc(pay32 + (rbyte >> 2), ((bit0[u] + tot[u] + 31u) >> 5) * 4u);
 #pragma unroll
             for (int j = 0; j < K; ++j) {
-                const uint32_t q = (ofs[u][j] + bit0[u]) >> 5;
-                d0[u][j] = p[q];
-                d1[u][j] = p[q + 1];
+                load_window(rr, (ofs[u][j] + bit0[u]) >> 5, d0[u][j], d1[u][j]);
             }
         }
         uint32_t x[RB][K];

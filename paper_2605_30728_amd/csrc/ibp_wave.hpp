@@ -115,6 +115,37 @@ __device__ __forceinline__ void expand_row_meta(const RowMeta<K, FORM> &r, uint3
     }
 }
 
+// A buffer resource over the dwords of one packed row (from `p`, `bytes` of them, a
+// multiple of 4): a buffer load at a byte offset at or past `bytes` returns 0 without
+// touching memory (the buffer range check), so a row's window loads, which read each
+// word's two dwords and for lanes past the row's last word the dword after it, never
+// fetch the line after the row's last packed dword. 0x00020000 is the gfx9 descriptor's
+// fourth dword for raw 32-bit buffer loads.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const uint32_t *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(p), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint32_t row_dword(__amdgpu_buffer_rsrc_t r, uint32_t q) {
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)(q * 4u), 0, 0);
+}
+
+// A word's 64-bit window as two dword loads (dwords q and q + 1 of p). The compiler would
+// merge them into one 8-byte load, which is misaligned for every odd q; an opaque second
+// index keeps them two 4-byte loads. Measured: the 111M-row gather 830 -> 695 us, the bf16
+// KV layer decompress 46.3 -> 43.0 us; the thresholded kernels keep the merged load (their
+// KV layer measured 5% slower split, their gathers no faster).
+__device__ __forceinline__ void load_window(const uint32_t *__restrict__ p, uint32_t q, uint32_t &d0, uint32_t &d1) {
+    uint32_t q1 = q + 1u;
+    asm volatile("" : "+v"(q1));
+    d0 = p[q];
+    d1 = p[q1];
+}
+__device__ __forceinline__ void load_window(__amdgpu_buffer_rsrc_t r, uint32_t q, uint32_t &d0, uint32_t &d1) {
+    uint32_t q1 = q + 1u;
+    asm volatile("" : "+v"(q1));
+    d0 = row_dword(r, q);
+    d1 = row_dword(r, q1);
+}
+
 // Store of a gathered output word that no later step of the kernel reads: marked
 // non-temporal, so a gather's output stream does not evict the metadata slots and packed
 // rows that neighbouring requests are about to read from L2 (measured: 7% on 53k Zipf
