@@ -120,7 +120,7 @@ def kernel_name(workload, W, part=False):
     if workload in GATHERS:
         rb = {1: 8, 2: 4, 4: 2, 8: 1}[k]
         return f"k_gather_rows<{k},{rb}>" if W <= 512 else "k_gather_tiled"
-    return f"k_decompress<{k},{ {1: 4, 2: 4, 4: 2, 8: 1}[k] }>"
+    return f"k_decompress<{k},{ {1: 4, 2: 4, 4: 2, 8: 1}[k] },true>"   # device payload: split window loads
 
 
 def measured_traffic(workload, part=False):

@@ -21,6 +21,8 @@ struct DevStream {
     uint32_t part_m;         // participation scheme: words per chunk; 0 = clustered scheme
     uint32_t row_align;      // clustered scheme: rows of a cluster start every
                              // roundup(rb, row_align) bytes (0: every rb bytes, no padding)
+    uint32_t payload_host;   // 1: the kernels read the payload in pinned host memory over
+                             // PCIe (zero-copy placements), 0: device memory (payload or stage)
     // clustered scheme, W <= 512, every cluster with at most 16 distinct (Mask, Bitval)
     // pairs: the row gathers' compact metadata, one slot of slot_bytes per cluster holding
     // slot_pairs (8 or 16) pairs and the 4-bit word indices (see load_row_meta); slots

@@ -731,6 +731,7 @@ ibp_status open_impl(const void *stream, uint64_t stream_bytes, int device, uint
     h->ds.g_magic = dev::div_magic(d.group_rows);
     h->ds.part_m = (d.flags & IBP_STREAM_PARTICIPATION) ? d.chunk_bytes / 4 : 0;
     h->ds.row_align = flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED ? (uint32_t)kRowAlign : 0;
+    h->ds.payload_host = flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY || flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED;
     h->ds.W = d.row_bytes / 4;
     h->ds.G = d.group_rows;
     ignore(hipSetDevice(prev));

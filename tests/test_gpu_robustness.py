@@ -168,12 +168,15 @@ def _leak_free_failures(torch, call, what, max_n=40):
 @pytest.mark.parametrize("placement", list(PLACEMENTS))
 @pytest.mark.parametrize("scheme", ["clustered", "participation"])
 def test_open_allocation_failures(torch, placement, scheme):
-    if scheme == "participation" and placement == "zero_copy_aligned":
-        pytest.skip("aligned rows hold clustered-scheme streams only")
     base = ibp.ibp_memory_usage()
     rows = structured_rows("floats", 500, 128, seed=5)
     stream = (oracle.compress(rows, 500, chunk_bytes=8, threshold=(4, 5)) if scheme == "participation"
               else oracle.compress(rows, 32))
+    if scheme == "participation" and placement == "zero_copy_aligned":
+        # aligned rows hold clustered-scheme streams only: refused before any allocation
+        st, hp = _raw_open(stream, PLACEMENTS[placement])
+        assert st == ibp.IBP_EINVAL and hp is None and ibp.ibp_memory_usage() == base
+        return
     opened = []
 
     def call():

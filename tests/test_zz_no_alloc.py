@@ -44,9 +44,12 @@ CASES = [("floats", 3000, 400, 32, "clustered"), ("sparse", 2000, 512, 64, "clus
 def test_noalloc_matches_allocating_gather(torch, kind, n, L, G, scheme, placement):
     rows = structured_rows(kind, n, L, seed=n + L)
     if scheme == "participation":
-        if placement == "zero_copy_aligned":
-            pytest.skip("aligned rows hold clustered-scheme streams only")
         stream = oracle.compress(rows, G, chunk_bytes=8, threshold=(4, 5))
+        if placement == "zero_copy_aligned":   # aligned rows hold clustered-scheme streams only
+            with pytest.raises(ibp.IbpError) as e:
+                ibp.ibp_open(stream, 0, PLACEMENTS[placement])
+            assert e.value.status == ibp.IBP_EINVAL
+            return
     else:
         stream = oracle.compress(rows, G)
     rng = np.random.default_rng(n * 7 + L)
