@@ -493,10 +493,29 @@ ibp_status gather_host_payload(ibp_handle *h, const int64_t *ids, uint64_t n, ui
     // the first bad position is reported before anything is enqueued
     const uint64_t n_rows = h->d.n_rows;
     std::atomic<uint64_t> first_bad{n};
+    // Every request reads its cluster's (or row's) offset and size at random places in
+    // host tables of tens of MB: prefetch them a few requests ahead, so that the misses
+    // overlap instead of following one another.
+    auto prefetch_meta = [&](uint64_t i) {
+        const uint64_t id = (uint64_t)ids[i];
+        if (id >= n_rows) return;
+        if (part) {
+            __builtin_prefetch(hoff + id);
+            __builtin_prefetch(hoff + id + 1);
+        } else {
+            const uint64_t g = G == 1 ? id : (uint64_t)(((unsigned __int128)id * magic) >> 64);
+            __builtin_prefetch(hoff + g);
+            __builtin_prefetch(grb + g);
+        }
+    };
     h->pool->run(nblk_all, 1, [&](uint64_t lo, uint64_t hi) {
+        constexpr uint64_t kAhead = 16;   // requests prefetched ahead
         for (uint64_t k = lo; k < hi; ++k) {
             uint64_t sum = 0;
-            for (uint64_t i = k * blk, e = std::min(n, i + blk); i < e; ++i) {
+            const uint64_t a = k * blk, e = std::min(n, a + blk);
+            for (uint64_t i = a; i < std::min(e, a + kAhead); ++i) prefetch_meta(i);
+            for (uint64_t i = a; i < e; ++i) {
+                if (i + kAhead < e) prefetch_meta(i + kAhead);
                 const uint64_t id = (uint64_t)ids[i];
                 if (id >= n_rows) {   // negative ids wrap to large values
                     uint64_t cur = first_bad.load(std::memory_order_relaxed);
