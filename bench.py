@@ -315,8 +315,9 @@ class Steps:
 def cpu_baseline(stream, rows, steps, last, L, G, seconds, compress_kw=None):
     """The oracle on this host's cores (one thread): decode of exactly the rows of whole
     steps, starting with the step the GPU ran last, until about `seconds` have passed; then
-    compress of the leading clusters of the tensor for about a third of that time (with
-    the stream's own scheme: compress_kw holds the participation-scheme parameters)."""
+    compress of whole clusters spread evenly over the tensor, at least 1% of them and more
+    while a third of that time allows (with the stream's own scheme: compress_kw holds the
+    participation-scheme parameters)."""
     kw = compress_kw or {}
     import oracle
     t0 = time.perf_counter()
@@ -331,23 +332,33 @@ def cpu_baseline(stream, rows, steps, last, L, G, seconds, compress_kw=None):
         if time.perf_counter() - t0 >= seconds or done_steps >= 4 * len(steps):
             break
     dec_s = time.perf_counter() - t0
-    # compress: leading clusters, sized from a first cluster's time
+    # compress: whole clusters spread evenly over the tensor (every k-th), as many as a third
+    # of the time budget allows and at least 1% of them; clusters compress independently
+    # (the thresholded scheme's sampled global Mask is drawn from these rows only)
     n_groups = (rows.shape[0] + G - 1) // G
     t = time.perf_counter()
     oracle.compress(rows[:G], G, **kw)
     per_group = max(time.perf_counter() - t, 1e-6)
-    ng = int(min(n_groups, max(1, seconds / 3 / per_group)))
-    m = min(rows.shape[0], ng * G)
+    ng = int(min(n_groups, max(1, seconds / 3 / per_group, -(-n_groups // 100))))
+    step = max(1, n_groups // ng)
+    picked = np.arange(0, n_groups, step)[:ng]
+    sel = np.concatenate([np.arange(g * G, min((g + 1) * G, rows.shape[0])) for g in picked]) \
+        if step > 1 else np.arange(min(rows.shape[0], ng * G))
+    sample = rows[sel]
+    m = sample.shape[0]
     t = time.perf_counter()
-    oracle.compress(rows[:m], G, **kw)
+    oracle.compress(sample, G, **kw)
     comp_s = time.perf_counter() - t
+    del sample
     log(f"[bench] cpu oracle: decode {done_rows * L / dec_s / 1e6:.1f} MB/s over {done_steps} step(s); "
         f"compress {m * L / comp_s / 1e6:.1f} MB/s over {ng} of {n_groups} clusters")
     return {"value": round(done_rows * L / dec_s / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"bit-serial oracle decode of the rows of {done_steps} whole step(s) "
                       f"({done_rows} rows, {dec_s:.1f} s, 1 thread)",
             "compress": {"GBps": round(m * L / comp_s / 1e9, 6),
-                         "sample": f"leading {ng} of {n_groups} clusters ({m} rows, {comp_s:.1f} s, 1 thread)"},
+                         "sample": (f"all {n_groups} clusters" if ng == n_groups else
+                                    f"{ng} of {n_groups} clusters, one in every {step}") +
+                                   f" ({m} rows, {comp_s:.1f} s, 1 thread)"},
             "host": host_info()}
 
 
