@@ -30,7 +30,17 @@ struct DevStream {
     const uint8_t *slots;
     uint32_t slot_pairs;
     uint32_t slot_bytes;
+    // participation scheme, rows of at most 65535 / kRowLineRows bytes: the row offsets
+    // line-packed, one 128-byte line per kRowLineRows rows (see row_span); null: the
+    // kernels read `index`
+    const uint8_t *row_lines;
+    uint64_t rl_magic;       // div_magic(kRowLineRows)
 };
+
+// Rows per line of DevStream::row_lines: line j holds the u64 payload offset of row
+// j * kRowLineRows, then for k = 1 .. kRowLineRows the u16 offset of row j * kRowLineRows + k
+// (of the payload end past the last row) relative to it: 8 + 2 * 60 = 128 bytes.
+inline constexpr uint32_t kRowLineRows = 60;
 
 uint64_t div_magic(uint32_t G);
 

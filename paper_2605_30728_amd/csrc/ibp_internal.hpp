@@ -100,4 +100,12 @@ constexpr uint64_t meta_slot_bytes(uint32_t pairs, uint32_t K) { return (8ull * 
 uint32_t build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, uint32_t K, Pool &pool,
                           std::vector<uint8_t> &slots);
 
+// Line-packed row offsets of a participation-scheme stream (ibp_meta_slots.cpp), from its
+// per-row index off[0..n_rows] (unaligned u64s at index_bytes): one 128-byte line per R
+// rows, line j holding off[jR] (u64) and then off[min(jR + k, n_rows)] - off[jR] for
+// k = 1..R (u16). Returns false (lines cleared) when a difference does not fit 16 bits
+// or 8 + 2R > 128.
+bool build_row_lines(const uint8_t *index_bytes, uint64_t n_rows, uint32_t R, Pool &pool,
+                     std::vector<uint8_t> &lines);
+
 }  // namespace ibp

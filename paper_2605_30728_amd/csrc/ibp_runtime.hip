@@ -191,6 +191,7 @@ struct ibp_handle {
     dev::DevStream ds{};
     uint32_t *d_meta = nullptr;
     uint8_t *d_slots = nullptr;           // compact metadata of the row gathers (clustered, W <= 512)
+    uint8_t *d_row_lines = nullptr;       // line-packed row offsets (participation, rows <= 1092 B)
     uint64_t *d_index = nullptr;
     uint8_t *d_payload = nullptr;
     const uint8_t *k_payload = nullptr;   // what the kernels read: d_payload or the pinned host payload
@@ -296,11 +297,13 @@ ibp_status check_handle(ibp_handle *h, const CallScope &cs) {
 void release_handle(ibp_handle *h) {
     dev_free(h->d_meta);
     dev_free(h->d_slots);
+    dev_free(h->d_row_lines);
     dev_free(h->d_index);
     dev_free(h->d_payload);
     dev_free(h->d_err);
     h->d_meta = nullptr;
     h->d_slots = nullptr;
+    h->d_row_lines = nullptr;
     h->d_index = nullptr;
     h->d_payload = nullptr;
     h->d_err = nullptr;
@@ -718,6 +721,18 @@ ibp_status open_impl(const void *stream, uint64_t stream_bytes, int device, uint
             h->ds.slot_bytes = (uint32_t)meta_slot_bytes(P, K);
         }
     }
+    if ((d.flags & IBP_STREAM_PARTICIPATION) && d.n_rows > 0 && d.n_rows <= ~0ull / dev::kRowLineRows &&
+        (uint64_t)d.row_bytes * dev::kRowLineRows <= 0xFFFF) {
+        // every row is at most row_bytes long (validated), so a line's 60 row ends fit u16
+        check_alloc();
+        std::vector<uint8_t> lines;
+        if (build_row_lines(v.index_bytes(), d.n_rows, dev::kRowLineRows, *h->pool, lines)) {
+            if (dev_alloc(&h->d_row_lines, lines.size()) != hipSuccess)
+                return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
+            if (hipMemcpy(h->d_row_lines, lines.data(), lines.size(), hipMemcpyHostToDevice) != hipSuccess)
+                return bail(fail(IBP_EHIP, "metadata upload failed"));
+        }
+    }
     if (flags == IBP_OPEN_PAYLOAD_DEVICE) {
         const uint64_t bytes = round_up(d.payload_bytes + kSlack, 256);
         if (dev_alloc(&h->d_payload, bytes) != hipSuccess)
@@ -744,6 +759,8 @@ ibp_status open_impl(const void *stream, uint64_t stream_bytes, int device, uint
     if (hipDeviceSynchronize() != hipSuccess) return bail(fail(IBP_EHIP, "upload did not complete"));
     h->ds.meta = h->d_meta;
     h->ds.slots = h->d_slots;
+    h->ds.row_lines = h->d_row_lines;
+    h->ds.rl_magic = dev::div_magic(dev::kRowLineRows);
     h->ds.index = h->d_index;
     h->ds.n_rows = d.n_rows;
     h->ds.n_groups = d.n_groups;

@@ -140,6 +140,42 @@ void check_slots(const std::vector<uint8_t> &stream, ibp::Pool &pool) {
     }
 }
 
+// The line-packed row offsets of a participation stream give back every row's span of
+// the per-row index, for the kernels' block of 60 rows and for short blocks that make
+// small streams span several lines.
+void check_row_lines(const std::vector<uint8_t> &stream, ibp::Pool &pool) {
+    ibp_desc d{};
+    if (ibp_describe(stream.data(), stream.size(), &d) != IBP_OK || d.flags == 0) return;
+    const uint8_t *index = stream.data() + d.index_off;
+    auto off = [&](uint64_t r) {
+        uint64_t v;
+        std::memcpy(&v, index + 8 * r, 8);
+        return v;
+    };
+    std::vector<uint8_t> lines;
+    CHECK(!ibp::build_row_lines(index, d.n_rows, 61, pool, lines), "61 rows do not fit a line");
+    for (uint32_t R : {1u, 3u, 60u}) {
+        const bool fits = (uint64_t)R * d.row_bytes <= 0xFFFF;
+        const bool built = ibp::build_row_lines(index, d.n_rows, R, pool, lines);
+        if (!built) {
+            CHECK(!fits, "row lines refused although R * row_bytes fits 16 bits");
+            continue;
+        }
+        CHECK(lines.size() >= (d.n_rows + R - 1) / R * 128, "row line area");
+        for (uint64_t r = 0; r < d.n_rows; ++r) {
+            const uint8_t *ln = lines.data() + (r / R) * 128;
+            const uint32_t k = (uint32_t)(r % R);
+            uint64_t base;
+            uint16_t e0 = 0, e1;
+            std::memcpy(&base, ln, 8);
+            if (k) std::memcpy(&e0, ln + 8 + 2ull * (k - 1), 2);
+            std::memcpy(&e1, ln + 8 + 2ull * k, 2);
+            CHECK(base + e0 == off(r) && base + e1 == off(r + 1), "row line span r=%llu R=%u",
+                  (unsigned long long)r, R);
+        }
+    }
+}
+
 void corrupt_describe(const std::vector<uint8_t> &stream, Rng &r) {
     ibp_desc d{};
     if (ibp_describe(stream.data(), stream.size(), &d) != IBP_OK) return;
@@ -263,6 +299,7 @@ int main() {
                         CHECK(pg == pw, "participation stream L=%u n=%llu kind=%d G=%u CS=%u T=%u/%u every=%u", L,
                               (unsigned long long)n, kind, G, CS, th.first, th.second, every);
                         roundtrip(rows, n, L, pw, true);
+                        check_row_lines(pw, pool);
                         if (r.next() % 4 == 0) corrupt_describe(pw, r);
                         ++cases;
                     }
