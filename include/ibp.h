@@ -209,7 +209,10 @@ ibp_status ibp_describe(const void *stream, uint64_t stream_bytes, ibp_desc *d);
  * serve every later decompression (Sec. 4: the invariant-bit metadata lives in GPU
  * memory for the whole dataset), and the payload goes to device memory or stays in
  * library-owned pinned host memory to be read over PCIe on demand (Sec. 5, PCIe transfer
- * compression; Sec. 4.4), see the flags.
+ * compression; Sec. 4.4), see the flags. Derived device copies are added where they
+ * serve the gathers: compact per-cluster metadata slots (clustered streams, rows of at
+ * most 2 KiB) and the per-row offsets packed 60 rows to a 128-byte line (thresholded
+ * streams, rows of at most 1,092 bytes); ibp_memory_usage reports the total.
  * The stream buffer is not referenced after ibp_open returns. *h receives a handle
  * owned by the library until ibp_close.
  * Errors: IBP_EINVAL, IBP_ECORRUPT, IBP_ENOMEM, IBP_EHIP.
