@@ -111,3 +111,42 @@ def test_gather_both_metadata_forms(torch, W, mode, pairs):
     got = out[:ids.size * L].cpu().numpy().reshape(ids.size, L)
     assert (out[ids.size * L:].cpu().numpy() == 0xA5).all(), "wrote past the output"
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("W", [16, 64, 100, 128, 200, 256, 500, 512])
+@pytest.mark.parametrize("mode", ["device_ids", "host_ids", "host_payload", "zero_copy"])
+@pytest.mark.parametrize("pairs", ["fit", "fit16", "mixed"])
+def test_participation_gather_both_metadata_forms(torch, W, mode, pairs):
+    """The thresholded scheme under per-cluster Masks over the same clusters: batches whose
+    rows lie in different clusters read every row's raw Mask/Bitval words (no slots for
+    this scheme; the slot's pair expansion measured slower there). With T = n (threshold
+    1/1) the per-cluster Masks are the clustered scheme's, so the same rows give the same
+    pair counts."""
+    G = 32
+    n = G * len(SETS[pairs]) * 2 + 5
+    L = 4 * W
+    rows = pair_rows(W, G, n, seed=W + 7, pairs=SETS[pairs])
+    counts = distinct_pairs(rows, G, W)
+    stream = oracle.compress(rows, G, chunk_bytes=4, threshold=(1, 1))
+    rng = np.random.default_rng(W + 3)
+    # unsorted ids put rows of different clusters into one batch; the sorted run and the
+    # full range give batches of one cluster too
+    ids = np.concatenate([rng.integers(0, n, size=3 * n), np.sort(rng.integers(0, n, size=n)),
+                          np.arange(n), [n - 1, 0]]).astype(np.int64)
+    want = oracle.decode_rows(stream, ids, L)
+    assert np.array_equal(want, rows[ids])
+    say(f"[part meta forms] W={W} mode={mode} n={n} ids={ids.size} pairs={sorted(set(counts))}")
+    flags = {"device_ids": ibp.IBP_OPEN_PAYLOAD_DEVICE, "host_ids": ibp.IBP_OPEN_PAYLOAD_DEVICE,
+             "host_payload": ibp.IBP_OPEN_PAYLOAD_HOST, "zero_copy": ibp.IBP_OPEN_PAYLOAD_HOST_ZERO_COPY}[mode]
+    out = torch.full((ids.size * L + 256,), 0xA5, dtype=torch.uint8, device="cuda")
+    with ibp.ibp_open(stream, 0, flags) as h:
+        assert ibp.ibp_get_stats(h)["gather_meta_bytes"] == 2 * L
+        if mode in ("device_ids", "zero_copy"):
+            ibp.ibp_gather_decompress_device(h, torch.from_numpy(ids).cuda(), out, out_cap=ids.size * L)
+        else:
+            ibp.ibp_gather_decompress(h, ids, out, out_cap=ids.size * L)
+        torch.cuda.synchronize()
+        assert ibp.ibp_device_errors(h) == 0
+    got = out[:ids.size * L].cpu().numpy().reshape(ids.size, L)
+    assert (out[ids.size * L:].cpu().numpy() == 0xA5).all(), "wrote past the output"
+    assert np.array_equal(got, want)
