@@ -444,8 +444,16 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
     for (uint32_t bb = 0; bb < nb; ++bb) {
         const uint32_t base_i = bb * RB;
         RowMeta<K, FORM> meta[RB];
+        // a row whose cluster is its predecessor's in the batch reuses that row's setup
+        // below, so only the batch's first row of each cluster loads the metadata
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
+            const bool same = u > 0 && (base_i + u >= cnt || ((samep >> ((base_i + u) & 63)) & 1ull));
+            if (same) {
+#pragma unroll
+                for (int k = 0; k < (int)(sizeof(meta[u].v) / sizeof(meta[u].v[0])); ++k) meta[u].v[k] = 0u;
+                continue;
+            }
             const uint64_t g = rd64(g_lo, g_hi, slot_of(base_i + u));
             load_row_meta<K, FORM>(meta[u], s.meta + g * 2ull * W, s.slots + g * s.slot_bytes, s.slot_pairs, W);
         }
