@@ -441,6 +441,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
         }
         pending = false;
     };
+    // the setup of the previous batch's last row, for a batch whose first row shares its
+    // cluster (sorted ids often continue a cluster across the batch boundary)
+    uint32_t c_nm[K] = {}, c_bv[K] = {}, c_ofs[K] = {}, c_nh = 0, c_tot = 0;
     for (uint32_t bb = 0; bb < nb; ++bb) {
         const uint32_t base_i = bb * RB;
         RowMeta<K, FORM> meta[RB];
@@ -448,7 +451,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
         // below, so only the batch's first row of each cluster loads the metadata
 #pragma unroll
         for (int u = 0; u < RB; ++u) {
-            const bool same = u > 0 && (base_i + u >= cnt || ((samep >> ((base_i + u) & 63)) & 1ull));
+            // base_i + u > 0: samep's bit compares the request with the one before it, which
+            // for u = 0 is the previous batch's last row
+            const bool same = base_i + u > 0 && (base_i + u >= cnt || ((samep >> ((base_i + u) & 63)) & 1ull));
             if (same) {
 #pragma unroll
                 for (int k = 0; k < (int)(sizeof(meta[u].v) / sizeof(meta[u].v[0])); ++k) meta[u].v[k] = 0u;
@@ -470,8 +475,17 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
             // sorted ids put rows of one cluster next to each other: a row whose cluster
             // is its predecessor's reuses that row's offsets and hole count (uniform branch;
             // slots past the end repeat the last request, so they always do)
-            const bool same = u > 0 && (base_i + u >= cnt || ((samep >> ((base_i + u) & 63)) & 1ull));
-            if (same) {
+            const bool same = base_i + u > 0 && (base_i + u >= cnt || ((samep >> ((base_i + u) & 63)) & 1ull));
+            if (same && u == 0) {
+#pragma unroll
+                for (int j = 0; j < K; ++j) {
+                    nm[u][j] = c_nm[j];
+                    bv[u][j] = c_bv[j];
+                    ofs[u][j] = c_ofs[j];
+                }
+                nh[u] = c_nh;
+                tot[u] = c_tot;
+            } else if (same) {
 #pragma unroll
                 for (int j = 0; j < K; ++j) {
                     nm[u][j] = nm[up][j];
@@ -522,6 +536,14 @@ __global__ __launch_bounds__(kBlock) void k_gather_rows(DevStream s, const uint3
         for (int u = 0; u < RB; ++u)
 #pragma unroll
             for (int j = 0; j < K; ++j) pv[u][j] = word_deposit(bv[u][j], nm[u][j], x[u][j], nh[u]);
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            c_nm[j] = nm[RB - 1][j];
+            c_bv[j] = bv[RB - 1][j];
+            c_ofs[j] = ofs[RB - 1][j];
+        }
+        c_nh = nh[RB - 1];
+        c_tot = tot[RB - 1];
         pbase = base_i;
         pending = true;
     }
