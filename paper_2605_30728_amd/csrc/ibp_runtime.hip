@@ -9,7 +9,11 @@
 //                                       IBP_OPEN_PAYLOAD_HOST_ZERO_COPY the kernels read
 //                                       the pinned host copy through its device address;
 //                                       with ..._ALIGNED that copy holds every row on a
-//                                       128-byte boundary and d_index its offsets)
+//                                       128-byte boundary and d_index its offsets). The
+//                                       device and zero-copy copies of a clustered stream
+//                                       whose rows are mostly whole 128-byte lines start
+//                                       every cluster on a line (line_aligned_clusters),
+//                                       d_index then holding those offsets
 // The kernels read a word's 64-bit window as two dwords at its bit offset, so every
 // payload buffer the kernels see (device payload or staging) has kSlack readable bytes
 // past its last packed byte.
@@ -370,16 +374,69 @@ ibp_status claim_ids(ibp_handle *h, int j, uint64_t n) {
     return IBP_OK;
 }
 
-ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
+// Line-aligned cluster layout of a clustered stream's payload, for the copies the kernels
+// read in place (device payload, zero-copy pinned payload): every cluster starts on a
+// 128-byte line, rows of a cluster back to back as in the stream. A cluster whose rows are
+// whole lines (rb a multiple of 128) then keeps every row on whole lines: in the stream one
+// cluster of 255-byte rows shifts all later rows by 64 bytes, and a 256-byte row 64 bytes
+// off a line boundary costs three line fetches instead of two. aoff receives the aligned
+// cluster offsets (n_groups + 1) and runs the first cluster of every stretch that keeps one
+// shift from the stream's offsets (copied as one piece), with n_groups at the end. Returns
+// false when fewer than half the clusters have rows of whole lines (the padding would buy
+// nothing) or the copy would take more than kMaxRuns pieces.
+constexpr uint64_t kMaxRuns = 4096;
+bool line_aligned_clusters(const StreamView &v, std::vector<uint64_t> &aoff, std::vector<uint64_t> &runs) {
+    const ibp_desc &d = v.d;
+    const uint64_t ng = d.n_groups;
+    if (d.flags != 0 || ng == 0) return false;
+    uint64_t whole = 0;
+    for (uint64_t g = 0; g < ng; ++g)
+        if ((v.off(g + 1) - v.off(g)) / v.rows_in_group(g) % kRowAlign == 0) ++whole;
+    if (2 * whole < ng) return false;
+    check_alloc();
+    aoff.assign(ng + 1, 0);
+    runs.assign(1, 0);
+    for (uint64_t g = 0; g < ng; ++g) {
+        const uint64_t end = aoff[g] + (v.off(g + 1) - v.off(g));
+        aoff[g + 1] = g + 1 < ng ? (end + kRowAlign - 1) / kRowAlign * kRowAlign : end;
+        if (g + 1 < ng && aoff[g + 1] - v.off(g + 1) != aoff[g] - v.off(g)) {
+            runs.push_back(g + 1);
+            if (runs.size() > kMaxRuns) return false;
+        }
+    }
+    runs.push_back(ng);
+    return true;
+}
+
+// The host payload of the PCIe placements (IBP_OPEN_PAYLOAD_HOST, _ZERO_COPY) in pinned
+// memory; `aoff`/`runs` (zero-copy only) give the line-aligned cluster layout, else the
+// stream's own byte layout is kept.
+ibp_status setup_host_path(ibp_handle *h, const StreamView &v, const std::vector<uint64_t> *aoff,
+                           const std::vector<uint64_t> &runs) {
     const ibp_desc &d = h->d;
-    if (pinned_alloc(&h->h_payload, d.payload_bytes + kSlack) != hipSuccess)
+    const uint64_t bytes = aoff ? (*aoff)[d.n_groups] : d.payload_bytes;
+    if (pinned_alloc(&h->h_payload, bytes + kSlack) != hipSuccess)
         return fail(IBP_ENOMEM, "pinned allocation for the payload failed");
     const uint8_t *src = v.payload();
     uint8_t *dst = h->h_payload;
-    h->pool->run(d.payload_bytes, 64ull << 20, [&](uint64_t lo, uint64_t hi) {
-        std::memcpy(dst + lo, src + lo, hi - lo);
-    });
-    std::memset(dst + d.payload_bytes, 0, kSlack);
+    if (!aoff) {
+        h->pool->run(d.payload_bytes, 64ull << 20, [&](uint64_t lo, uint64_t hi) {
+            std::memcpy(dst + lo, src + lo, hi - lo);
+        });
+    } else {
+        // each stretch in one piece (its bytes keep their order), then the padding between
+        // stretches zeroed
+        for (size_t k = 0; k + 1 < runs.size(); ++k) {
+            const uint64_t g0 = runs[k], g1 = runs[k + 1];
+            const uint64_t s0 = v.off(g0), n = v.off(g1) - s0, d0 = (*aoff)[g0];
+            h->pool->run(n, 64ull << 20, [&](uint64_t lo, uint64_t hi) {
+                std::memcpy(dst + d0 + lo, src + s0 + lo, hi - lo);
+            });
+            const uint64_t next = g1 < d.n_groups ? (*aoff)[g1] : d0 + n;
+            std::memset(dst + d0 + n, 0, next - (d0 + n));
+        }
+    }
+    std::memset(dst + bytes, 0, kSlack);
     check_alloc();
     if (d.flags & IBP_STREAM_PARTICIPATION) {
         h->h_off.resize(d.n_rows + 1);
@@ -388,9 +445,9 @@ ibp_status setup_host_path(ibp_handle *h, const StreamView &v) {
     } else {
         h->h_off.resize(d.n_groups + 1);
         h->h_rb.resize(d.n_groups);
-        for (uint64_t g = 0; g <= d.n_groups; ++g) h->h_off[g] = v.off(g);
+        for (uint64_t g = 0; g <= d.n_groups; ++g) h->h_off[g] = aoff ? (*aoff)[g] : v.off(g);
         for (uint64_t g = 0; g < d.n_groups; ++g) {
-            h->h_rb[g] = (uint32_t)((h->h_off[g + 1] - h->h_off[g]) / v.rows_in_group(g));
+            h->h_rb[g] = (uint32_t)((v.off(g + 1) - v.off(g)) / v.rows_in_group(g));
             h->max_rb = std::max(h->max_rb, h->h_rb[g]);
         }
     }
@@ -701,7 +758,13 @@ ibp_status open_impl(const void *stream, uint64_t stream_bytes, int device, uint
         return bail(fail(IBP_ENOMEM, "device allocation for metadata failed"));
     if (meta_bytes && hipMemcpy(h->d_meta, v.meta(), meta_bytes, hipMemcpyHostToDevice) != hipSuccess)
         return bail(fail(IBP_EHIP, "metadata upload failed"));
-    if (hipMemcpy(h->d_index, v.index_bytes(), 8 * n_index, hipMemcpyHostToDevice) != hipSuccess ||
+    // the payload copies the kernels read in place (device, zero-copy) start every cluster
+    // on a 128-byte line when that keeps rows on whole lines (line_aligned_clusters)
+    std::vector<uint64_t> aoff, runs;
+    const bool line_al = (flags == IBP_OPEN_PAYLOAD_DEVICE || flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) &&
+                         line_aligned_clusters(v, aoff, runs);
+    if (hipMemcpy(h->d_index, line_al ? static_cast<const void *>(aoff.data()) : v.index_bytes(), 8 * n_index,
+                  hipMemcpyHostToDevice) != hipSuccess ||
         hipMemset(h->d_err, 0, 8) != hipSuccess)
         return bail(fail(IBP_EHIP, "index upload failed"));
     const uint32_t W = d.row_bytes / 4;
@@ -734,17 +797,30 @@ ibp_status open_impl(const void *stream, uint64_t stream_bytes, int device, uint
         }
     }
     if (flags == IBP_OPEN_PAYLOAD_DEVICE) {
-        const uint64_t bytes = round_up(d.payload_bytes + kSlack, 256);
+        const uint64_t used = line_al ? aoff[d.n_groups] : d.payload_bytes;
+        const uint64_t bytes = round_up(used + kSlack, 256);
         if (dev_alloc(&h->d_payload, bytes) != hipSuccess)
             return bail(fail(IBP_ENOMEM, "device allocation for the payload failed"));
-        if (hipMemset(h->d_payload + d.payload_bytes, 0, bytes - d.payload_bytes) != hipSuccess ||
-            (d.payload_bytes &&
-             hipMemcpy(h->d_payload, v.payload(), d.payload_bytes, hipMemcpyHostToDevice) != hipSuccess))
-            return bail(fail(IBP_EHIP, "payload upload failed"));
+        if (!line_al) {
+            if (hipMemset(h->d_payload + d.payload_bytes, 0, bytes - d.payload_bytes) != hipSuccess ||
+                (d.payload_bytes &&
+                 hipMemcpy(h->d_payload, v.payload(), d.payload_bytes, hipMemcpyHostToDevice) != hipSuccess))
+                return bail(fail(IBP_EHIP, "payload upload failed"));
+        } else {
+            // padding and slack zeroed, then every stretch of clusters in one copy
+            if (hipMemset(h->d_payload, 0, bytes) != hipSuccess)
+                return bail(fail(IBP_EHIP, "payload upload failed"));
+            for (size_t k = 0; k + 1 < runs.size(); ++k) {
+                const uint64_t s0 = v.off(runs[k]), n = v.off(runs[k + 1]) - s0;
+                if (n && hipMemcpy(h->d_payload + aoff[runs[k]], v.payload() + s0, n, hipMemcpyHostToDevice) !=
+                             hipSuccess)
+                    return bail(fail(IBP_EHIP, "payload upload failed"));
+            }
+        }
         h->k_payload = h->d_payload;
     } else {
         st = flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED ? setup_aligned_host_payload(h, v)
-                                                             : setup_host_path(h, v);
+                                                             : setup_host_path(h, v, line_al ? &aoff : nullptr, runs);
         if (st != IBP_OK) return bail(st);
         if (flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY || flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY_ALIGNED) {
             void *dp = nullptr;
