@@ -212,7 +212,11 @@ ibp_status ibp_describe(const void *stream, uint64_t stream_bytes, ibp_desc *d);
  * compression; Sec. 4.4), see the flags. Derived device copies are added where they
  * serve the gathers: compact per-cluster metadata slots (clustered streams, rows of at
  * most 2 KiB) and the per-row offsets packed 60 rows to a 128-byte line (thresholded
- * streams, rows of at most 1,092 bytes); ibp_memory_usage reports the total.
+ * streams, rows of at most 1,092 bytes); ibp_memory_usage reports the total. The payload
+ * copies the kernels read in place (device, zero-copy) of a clustered stream whose rows
+ * are mostly whole 128-byte lines start every cluster on a line (at most 127 bytes of
+ * padding per cluster), so one cluster of odd-sized rows does not shift later rows off
+ * the lines.
  * The stream buffer is not referenced after ibp_open returns. *h receives a handle
  * owned by the library until ibp_close.
  * Errors: IBP_EINVAL, IBP_ECORRUPT, IBP_ENOMEM, IBP_EHIP.
