@@ -108,4 +108,18 @@ uint32_t build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, ui
 bool build_row_lines(const uint8_t *index_bytes, uint64_t n_rows, uint32_t R, Pool &pool,
                      std::vector<uint8_t> &lines);
 
+// Line-aligned cluster layout of a clustered stream's payload (ibp_meta_slots.cpp), for the
+// copies the kernels read in place (device payload, zero-copy pinned payload): every cluster
+// starts on a `line`-byte boundary, rows of a cluster back to back as in the stream. A
+// cluster whose rows are whole lines (rb a multiple of `line`) then keeps every row on whole
+// lines: in the stream one cluster of 255-byte rows shifts all later rows by 64 bytes, and a
+// 256-byte row 64 bytes off a 128-byte line costs three line fetches instead of two. aoff
+// receives the aligned cluster offsets (n_groups + 1); runs the first cluster of every
+// stretch that keeps one shift from the stream's offsets (copied as one piece), then
+// n_groups. Returns false when fewer than half the clusters have rows of whole lines (the
+// padding would buy nothing), when the copy would take more than max_runs pieces, or for
+// a thresholded stream.
+bool line_aligned_clusters(const StreamView &v, uint64_t line, uint64_t max_runs, std::vector<uint64_t> &aoff,
+                           std::vector<uint64_t> &runs);
+
 }  // namespace ibp

@@ -23,6 +23,10 @@
 // fits one (a per-row choice of form would cost every row a branch); a stream with a
 // cluster of more than 16 pairs gets no slots and the raw words are read.
 //
+// The payload copies the kernels read in place may also start every cluster on a 128-byte
+// line (line_aligned_clusters), so that one cluster of odd-sized rows does not shift the
+// rows of whole lines after it across line boundaries.
+//
 // The participation scheme's per-row index gets a line-packed copy as well
 // (build_row_lines): a gather request then reads one 128-byte line holding its row's
 // offset and end instead of two u64 index entries, and the sparse requests of a batch
@@ -109,6 +113,30 @@ uint32_t build_meta_slots(const uint8_t *meta, uint64_t n_groups, uint32_t W, ui
         }
     });
     return P;
+}
+
+bool line_aligned_clusters(const StreamView &v, uint64_t line, uint64_t max_runs, std::vector<uint64_t> &aoff,
+                           std::vector<uint64_t> &runs) {
+    const ibp_desc &d = v.d;
+    const uint64_t ng = d.n_groups;
+    if (d.flags != 0 || ng == 0 || line == 0) return false;
+    uint64_t whole = 0;
+    for (uint64_t g = 0; g < ng; ++g)
+        if ((v.off(g + 1) - v.off(g)) / v.rows_in_group(g) % line == 0) ++whole;
+    if (2 * whole < ng) return false;
+    check_alloc();
+    aoff.assign(ng + 1, 0);
+    runs.assign(1, 0);
+    for (uint64_t g = 0; g < ng; ++g) {
+        const uint64_t end = aoff[g] + (v.off(g + 1) - v.off(g));
+        aoff[g + 1] = g + 1 < ng ? (end + line - 1) / line * line : end;
+        if (g + 1 < ng && aoff[g + 1] - v.off(g + 1) != aoff[g] - v.off(g)) {
+            runs.push_back(g + 1);
+            if (runs.size() > max_runs) return false;
+        }
+    }
+    runs.push_back(ng);
+    return true;
 }
 
 bool build_row_lines(const uint8_t *index_bytes, uint64_t n_rows, uint32_t R, Pool &pool,

@@ -54,6 +54,7 @@ constexpr uint64_t kStageBytes = 128ull << 20;   // one staging buffer (a whole 
 constexpr int kStages = 3;                        // staging buffers in rotation
 constexpr int kIdSlots = 2;                       // host-id buffers in rotation
 constexpr uint64_t kRowAlign = 128;               // PCIe line: row start of aligned zero-copy
+constexpr uint64_t kMaxRuns = 4096;               // copy pieces of a line-aligned cluster layout
 constexpr uint64_t kCountBytes = dev::kCountLines * dev::kCountStride * 8;   // cache counters
 constexpr uint64_t kBlk = 256;                    // rows per host packing task (a chunk
                                                   // holds tens of them, for 16 threads)
@@ -372,40 +373,6 @@ ibp_status claim_ids(ibp_handle *h, int j, uint64_t n) {
     }
     h->ids_cap[j] = cap;
     return IBP_OK;
-}
-
-// Line-aligned cluster layout of a clustered stream's payload, for the copies the kernels
-// read in place (device payload, zero-copy pinned payload): every cluster starts on a
-// 128-byte line, rows of a cluster back to back as in the stream. A cluster whose rows are
-// whole lines (rb a multiple of 128) then keeps every row on whole lines: in the stream one
-// cluster of 255-byte rows shifts all later rows by 64 bytes, and a 256-byte row 64 bytes
-// off a line boundary costs three line fetches instead of two. aoff receives the aligned
-// cluster offsets (n_groups + 1) and runs the first cluster of every stretch that keeps one
-// shift from the stream's offsets (copied as one piece), with n_groups at the end. Returns
-// false when fewer than half the clusters have rows of whole lines (the padding would buy
-// nothing) or the copy would take more than kMaxRuns pieces.
-constexpr uint64_t kMaxRuns = 4096;
-bool line_aligned_clusters(const StreamView &v, std::vector<uint64_t> &aoff, std::vector<uint64_t> &runs) {
-    const ibp_desc &d = v.d;
-    const uint64_t ng = d.n_groups;
-    if (d.flags != 0 || ng == 0) return false;
-    uint64_t whole = 0;
-    for (uint64_t g = 0; g < ng; ++g)
-        if ((v.off(g + 1) - v.off(g)) / v.rows_in_group(g) % kRowAlign == 0) ++whole;
-    if (2 * whole < ng) return false;
-    check_alloc();
-    aoff.assign(ng + 1, 0);
-    runs.assign(1, 0);
-    for (uint64_t g = 0; g < ng; ++g) {
-        const uint64_t end = aoff[g] + (v.off(g + 1) - v.off(g));
-        aoff[g + 1] = g + 1 < ng ? (end + kRowAlign - 1) / kRowAlign * kRowAlign : end;
-        if (g + 1 < ng && aoff[g + 1] - v.off(g + 1) != aoff[g] - v.off(g)) {
-            runs.push_back(g + 1);
-            if (runs.size() > kMaxRuns) return false;
-        }
-    }
-    runs.push_back(ng);
-    return true;
 }
 
 // The host payload of the PCIe placements (IBP_OPEN_PAYLOAD_HOST, _ZERO_COPY) in pinned
@@ -762,7 +729,7 @@ ibp_status open_impl(const void *stream, uint64_t stream_bytes, int device, uint
     // on a 128-byte line when that keeps rows on whole lines (line_aligned_clusters)
     std::vector<uint64_t> aoff, runs;
     const bool line_al = (flags == IBP_OPEN_PAYLOAD_DEVICE || flags == IBP_OPEN_PAYLOAD_HOST_ZERO_COPY) &&
-                         line_aligned_clusters(v, aoff, runs);
+                         line_aligned_clusters(v, kRowAlign, kMaxRuns, aoff, runs);
     if (hipMemcpy(h->d_index, line_al ? static_cast<const void *>(aoff.data()) : v.index_bytes(), 8 * n_index,
                   hipMemcpyHostToDevice) != hipSuccess ||
         hipMemset(h->d_err, 0, 8) != hipSuccess)

@@ -176,6 +176,42 @@ void check_row_lines(const std::vector<uint8_t> &stream, ibp::Pool &pool) {
     }
 }
 
+// The line-aligned cluster layout: every cluster starts on a line, each has room for its
+// packed rows, the last ends right after its rows, and the copy pieces cover the clusters
+// in order, each keeping one shift from the stream's offsets. Small lines make the small
+// streams here engage it; a limit of one piece exercises the refusal.
+void check_line_layout(const std::vector<uint8_t> &stream) {
+    ibp::StreamView v;
+    if (ibp::parse_stream(stream.data(), stream.size(), v) != IBP_OK || v.d.flags != 0 || v.d.n_groups == 0) return;
+    const uint64_t ng = v.d.n_groups;
+    for (uint64_t line : {4ull, 16ull, 128ull}) {
+        uint64_t whole = 0;
+        for (uint64_t g = 0; g < ng; ++g)
+            if ((v.off(g + 1) - v.off(g)) / v.rows_in_group(g) % line == 0) ++whole;
+        std::vector<uint64_t> aoff, runs;
+        const bool on = ibp::line_aligned_clusters(v, line, 1u << 20, aoff, runs);
+        CHECK(on == (2 * whole >= ng), "line layout engaged iff half the clusters have whole-line rows");
+        if (!on) continue;
+        CHECK(aoff.size() == ng + 1 && aoff[0] == 0 && runs.front() == 0 && runs.back() == ng, "layout shape");
+        for (uint64_t g = 0; g < ng; ++g) {
+            const uint64_t size = v.off(g + 1) - v.off(g);
+            CHECK(aoff[g] % line == 0, "cluster %llu not on a line", (unsigned long long)g);
+            if (g + 1 < ng)
+                CHECK(aoff[g + 1] == (aoff[g] + size + line - 1) / line * line, "cluster %llu end", (unsigned long long)g);
+            else
+                CHECK(aoff[g + 1] == aoff[g] + size, "last cluster end");
+        }
+        for (size_t k = 0; k + 1 < runs.size(); ++k) {
+            CHECK(runs[k] < runs[k + 1], "pieces in order");
+            for (uint64_t g = runs[k]; g < runs[k + 1]; ++g)
+                CHECK(aoff[g] - v.off(g) == aoff[runs[k]] - v.off(runs[k]), "one shift per piece");
+            if (k > 0)
+                CHECK(aoff[runs[k]] - v.off(runs[k]) != aoff[runs[k] - 1] - v.off(runs[k] - 1), "piece boundary");
+        }
+        if (runs.size() > 2) CHECK(!ibp::line_aligned_clusters(v, line, 1, aoff, runs), "piece limit");
+    }
+}
+
 void corrupt_describe(const std::vector<uint8_t> &stream, Rng &r) {
     ibp_desc d{};
     if (ibp_describe(stream.data(), stream.size(), &d) != IBP_OK) return;
@@ -283,6 +319,7 @@ int main() {
                     }
                     roundtrip(rows, n, L, want, false);
                     check_slots(want, pool);
+                    check_line_layout(want);
                     if (r.next() % 4 == 0) corrupt_describe(want, r);
                     ++cases;
                     // two seeded variants of the thresholded scheme per case
