@@ -60,12 +60,12 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decompressed GB/s (HBM roofline %) + effective H2D GB/s vs raw PCIe"
 HBM_PEAK_GBS = 8000.0
-# the sources the profiled kernels are compiled from, and the runtime that lays out the
-# data they read (a profile's counters stand only while these hash to the value recorded
-# with them)
+# the sources the profiled kernels are compiled from, and the runtime and layout builders
+# that lay out the data they read (a profile's counters stand only while these hash to the
+# value recorded with them)
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2605_30728_amd", "csrc", f)
                   for f in ("ibp_kernels.hip", "ibp_cache_kernels.hip", "ibp_wave.hpp", "ibp_device.hpp",
-                            "ibp_runtime.hip")]
+                            "ibp_runtime.hip", "ibp_meta_slots.cpp")]
 
 
 def code_sha256(texts):
