@@ -46,6 +46,7 @@ and prints one JSON line holding every point. `--cache` compares the compressed 
 cache with an uncompressed one of the same slab bytes (and no cache) on a gather workload.
 """
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -721,6 +722,11 @@ def main():
                 others[wl] = {"skipped": f"time budget ({left:.0f} s left of --budget-s {args.budget_s:.0f})"}
                 log(f"[bench] {wl}: skipped, {left:.0f} s left")
                 continue
+            # the previous workload's host and pinned memory (over 100 GB after the headline)
+            # is handed back to the system first: while that runs, host-bound legs measured
+            # several times slower (the 2 MiB tensor's staged copies: 9-23 GB/s against ~60)
+            gc.collect()
+            time.sleep(3.0)
             # at least 200 timed steps: the short lookups of the DLRM batches need that many
             # to reach their steady state (20 steps read ~60% slower), and they cost ~5 ms
             k_w, w_w = max(args.steps, 200), max(args.warmup, 20)
