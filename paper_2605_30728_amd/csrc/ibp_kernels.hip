@@ -357,7 +357,9 @@ __global__ __launch_bounds__(kBlock) void k_gather_tiled(DevStream s, const uint
 // A wave owns `seg` requests (lane i loads request i's id and cluster offset, once) and
 // decodes them RB rows at a time, each row independently: its cluster's metadata (compact
 // slot or Mask/Bitval words), a wave scan of popcount(~Mask) for the bit offsets, then its
-// packed windows. All metadata loads of a batch leave together, then all its window loads.
+// packed windows. All metadata loads of a batch leave together, then all its window loads;
+// a row in its predecessor's cluster (also the previous batch's last row) loads no
+// metadata and reuses that row's setup.
 // One batch per wave measured fastest at the gathers' sizes: prefetching the next batch's
 // metadata during the current batch's windows keeps its registers live through the
 // rebuild, and the lost occupancy costs more than the overlap gains. Rows are rebuilt with
