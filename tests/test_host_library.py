@@ -3,6 +3,7 @@ to the oracle's, its validation must reject corrupted streams, and the C ABI mus
 every entry point that include/ibp.h declares."""
 import os
 import re
+import sys
 
 import numpy as np
 import pytest
@@ -192,6 +193,31 @@ def test_kernel_code_hash_ignores_comments_only():
     assert bench.code_sha256([src]) == bench.code_sha256([same])
     assert bench.code_sha256([src]) != bench.code_sha256([other])
     assert len(bench.kernel_sources_sha256()) == 64
+
+
+def test_traffic_gate_reads_the_profile_only_while_the_code_matches(monkeypatch):
+    """bench.py reports a kernel's measured HBM traffic from its committed rocprofv3 summary
+    only while the hashed sources match the hash recorded there; any other hash, or a
+    profile without the two lines, gives None (the line then carries traffic null)."""
+    import bench
+    text = open(os.path.join(bench.ROOT, "profiles", "k_gather_rows_big_gnn.md")).read()
+    want = int(re.search(r"traffic_bytes_per_launch:\s*(\d+)", text).group(1))
+    recorded = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text).group(1)
+    monkeypatch.setattr(bench, "kernel_sources_sha256", lambda: recorded)
+    assert bench.measured_traffic("big_gnn") == want
+    monkeypatch.setattr(bench, "kernel_sources_sha256", lambda: "0" * 64)
+    assert bench.measured_traffic("big_gnn") is None
+    assert bench.measured_traffic("no_such_workload") is None
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus 2 exits with status 2 and says why, before any
+    device work."""
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU" in r.stdout + r.stderr
 
 
 def test_binding_rejects_host_buffers_for_device_arguments():
