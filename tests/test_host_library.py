@@ -210,6 +210,19 @@ def test_traffic_gate_reads_the_profile_only_while_the_code_matches(monkeypatch)
     assert bench.measured_traffic("no_such_workload") is None
 
 
+@pytest.mark.skipif(__import__("shutil").which("gcc") is None, reason="needs gcc")
+def test_header_is_plain_c():
+    """include/ibp.h is a C ABI: it compiles as pedantic C99 (and as C++), with no torch or
+    HIP types in it."""
+    import subprocess
+    for cmd in (["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only", "-x", "c", HEADER],
+                ["g++", "-std=c++11", "-Wall", "-Werror", "-fsyntax-only", "-x", "c++", HEADER]):
+        r = subprocess.run(cmd, capture_output=True, text=True, timeout=120)
+        assert r.returncode == 0, r.stderr
+    text = open(HEADER).read()
+    assert "torch" not in text.lower().replace("pytorch", "") and "hip_runtime" not in text
+
+
 def test_bench_refuses_more_than_one_gpu():
     """bench.py measures one GPU: --gpus 2 exits with status 2 and says why, before any
     device work."""
